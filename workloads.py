@@ -1,0 +1,323 @@
+"""Seeded synthetic workloads for the mixed block-decode / prefill attention call.
+
+This module only draws inputs. It holds none of the attention arithmetic, so
+both the fp64 oracle (``oracle/``) and the HIP path may use it.
+
+Shapes follow the paper's setting: bf16 serving (Sec. 6.1), KV pages of 16
+tokens and decode blocks of 32 positions (Sec. 6.1), prompts followed by the
+whole appended masked response (Sec. 6.1, trace setup), LLaDA-8B (MHA) and
+Dream-7B (GQA) head layouts (Sec. 6.1, Sec. 6.3). The paper's traces are not
+used: prompt lengths are drawn from lognormals whose medians and spreads stand
+in for Table 1.
+
+Recipe (one for every workload):
+
+1. ``numpy.random.default_rng(seed)`` draws, in this order, prompt lengths,
+   decode block indices and the page permutation.
+2. Prompt length ``P = clip(rint(exp(N(ln median, sigma))), lo, hi)``; context
+   length ``L = P + R`` (R = appended response length).
+3. A block decode at block index ``b`` has ``n = 32`` query rows at
+   positions ``o = P + 32 b``; a prefill has ``o = 0``, ``n = L``.
+4. Page ids are ``rng.permutation(pool)[:needed]``, handed out in item order.
+5. Values: each tensor piece has its own ``torch.Generator`` seeded from
+   (seed, item, kind); ``randn`` in fp32, then rounded to bf16 (RNE). The bf16
+   bytes are the ground truth both sides read.
+6. Batch order: decodes first, then prefills (the microbatch order of the
+   deficit scheduler, Alg. 1).
+"""
+from __future__ import annotations
+
+import dataclasses
+import math
+from typing import Callable, List, Optional, Tuple
+
+import numpy as np
+import torch
+
+PAGE_SIZE = 16
+BLOCK = 32
+
+# kinds of value tensors, used to derive per-piece seeds
+KIND_Q, KIND_KCTX, KIND_VCTX, KIND_KNEW, KIND_VNEW = range(5)
+
+
+@dataclasses.dataclass
+class Workload:
+    """Descriptor of one attention call plus deterministic value generators."""
+
+    name: str
+    seed: int
+    num_q_heads: int
+    num_kv_heads: int
+    head_dim: int
+    q_indptr: np.ndarray  # int32 [n+1]
+    q_offset: np.ndarray  # int32 [n]
+    kv_len: np.ndarray  # int32 [n]
+    is_prefill: np.ndarray  # bool [n]
+    page_indptr: np.ndarray  # int32 [n+1]
+    page_ids: np.ndarray  # int32 [page_indptr[-1]]
+    num_pool_pages: int
+    sm_scale: float  # float32 value
+    q_scale: float = 1.0  # stress variant multiplies Q by this before rounding
+    # optional overrides: item -> callable(kind) -> fp32 tensor
+    value_fn: Optional[Callable[[int, int], torch.Tensor]] = None
+    page_size: int = PAGE_SIZE
+
+    @property
+    def num_items(self) -> int:
+        return int(self.q_offset.shape[0])
+
+    @property
+    def total_q(self) -> int:
+        return int(self.q_indptr[-1])
+
+    def n(self, i: int) -> int:
+        return int(self.q_indptr[i + 1] - self.q_indptr[i])
+
+    # ------------------------------------------------------------------ values
+    def _gen(self, item: int, kind: int) -> torch.Generator:
+        g = torch.Generator(device="cpu")
+        mix = (((self.seed * 1_000_003) + item) * 8 + kind) & ((1 << 62) - 1)
+        g.manual_seed(mix)
+        return g
+
+    def _draw(self, item: int, kind: int, shape: Tuple[int, ...]) -> torch.Tensor:
+        if self.value_fn is not None:
+            t = self.value_fn(item, kind)
+            if t is not None:
+                assert tuple(t.shape) == tuple(shape), (t.shape, shape)
+                return t.to(torch.bfloat16)
+        x = torch.randn(shape, generator=self._gen(item, kind), dtype=torch.float32)
+        if kind == KIND_Q and self.q_scale != 1.0:
+            x = x * self.q_scale
+        return x.to(torch.bfloat16)
+
+    def q(self, i: int) -> torch.Tensor:
+        """Query rows of item i, bf16 [n_i, Hq, D]."""
+        return self._draw(i, KIND_Q, (self.n(i), self.num_q_heads, self.head_dim))
+
+    def k_new(self, i: int) -> torch.Tensor:
+        """Fresh keys of item i (positions o_i .. o_i+n_i-1), bf16 [n_i, Hkv, D]."""
+        return self._draw(i, KIND_KNEW, (self.n(i), self.num_kv_heads, self.head_dim))
+
+    def v_new(self, i: int) -> torch.Tensor:
+        return self._draw(i, KIND_VNEW, (self.n(i), self.num_kv_heads, self.head_dim))
+
+    def k_ctx(self, i: int) -> Optional[torch.Tensor]:
+        """Cache content before the call for positions [0, L_i), bf16 [L_i, Hkv, D].
+
+        None for a prefill (it brings its whole sequence as fresh rows). Rows
+        [o_i, o_i+n_i) hold stale values that the call must overwrite."""
+        if self.is_prefill[i]:
+            return None
+        return self._draw(i, KIND_KCTX, (int(self.kv_len[i]), self.num_kv_heads, self.head_dim))
+
+    def v_ctx(self, i: int) -> Optional[torch.Tensor]:
+        if self.is_prefill[i]:
+            return None
+        return self._draw(i, KIND_VCTX, (int(self.kv_len[i]), self.num_kv_heads, self.head_dim))
+
+    # ------------------------------------------------------- packed host views
+    def packed_q(self) -> torch.Tensor:
+        return torch.cat([self.q(i) for i in range(self.num_items)], 0)
+
+    def packed_k_new(self) -> torch.Tensor:
+        return torch.cat([self.k_new(i) for i in range(self.num_items)], 0)
+
+    def packed_v_new(self) -> torch.Tensor:
+        return torch.cat([self.v_new(i) for i in range(self.num_items)], 0)
+
+    def item_pages(self, i: int) -> np.ndarray:
+        return self.page_ids[self.page_indptr[i]:self.page_indptr[i + 1]]
+
+    def fill_paged_cache(self, k_pool: torch.Tensor, v_pool: torch.Tensor, items=None) -> None:
+        """Scatter each decode item's pre-call context into its pages.
+
+        Pool layout [num_pool_pages, Hkv, page_size, D]: position p of item i
+        lives in page page_ids[page_indptr[i] + p // page_size], slot
+        p % page_size. Works for CPU or device pools (copies per item)."""
+        S = self.page_size
+        for i in range(self.num_items) if items is None else items:
+            if self.is_prefill[i]:
+                continue
+            L = int(self.kv_len[i])
+            pages = torch.from_numpy(self.item_pages(i).astype(np.int64))
+            npg = pages.numel()
+            for kind, pool in ((KIND_KCTX, k_pool), (KIND_VCTX, v_pool)):
+                ctx = self.k_ctx(i) if kind == KIND_KCTX else self.v_ctx(i)
+                pad = torch.zeros((npg * S, self.num_kv_heads, self.head_dim), dtype=torch.bfloat16)
+                pad[:L] = ctx
+                # [npg, S, Hkv, D] -> [npg, Hkv, S, D]
+                blk = pad.view(npg, S, self.num_kv_heads, self.head_dim).permute(0, 2, 1, 3)
+                full = npg * S == L
+                dev_pages = pages.to(pool.device)
+                if full:
+                    pool[dev_pages] = blk.to(pool.device)
+                else:
+                    # the last page's slots >= L keep whatever the pool held
+                    pool[dev_pages[:-1]] = blk[:-1].to(pool.device)
+                    r = L - (npg - 1) * S
+                    pool[dev_pages[-1], :, :r] = blk[-1, :, :r].to(pool.device)
+
+    def flops(self) -> float:
+        """Algorithmic flops: QK^T and PV, non-causal, 4*n*L*D*Hq per item."""
+        n = np.diff(self.q_indptr).astype(np.float64)
+        return float(np.sum(4.0 * n * self.kv_len.astype(np.float64) * self.head_dim * self.num_q_heads))
+
+    def hbm_bytes(self) -> float:
+        """Algorithmic HBM bytes: K and V read once per item, the cache write of
+        the fresh rows, Q read, O write, page ids and the LSE write."""
+        n = np.diff(self.q_indptr).astype(np.float64)
+        L = self.kv_len.astype(np.float64)
+        D, Hq, Hkv = self.head_dim, self.num_q_heads, self.num_kv_heads
+        per = 2.0 * (2 * L * Hkv * D + 2 * n * Hkv * D + 2 * n * Hq * D)
+        per += 4.0 * np.ceil(L / self.page_size) + 4.0 * n * Hq
+        return float(np.sum(per))
+
+
+# ---------------------------------------------------------------- builders
+def _lognormal_lengths(rng, count, median, sigma, lo, hi) -> np.ndarray:
+    x = rng.normal(math.log(median), sigma, size=count)
+    return np.clip(np.rint(np.exp(x)), lo, hi).astype(np.int64)
+
+
+def make_workload(name: str, seed: int, *, hq: int, hkv: int, d: int,
+                  decodes: List[Tuple[int, int]], prefills: List[int],
+                  rng: Optional[np.random.Generator] = None, pool_pages: Optional[int] = None,
+                  q_scale: float = 1.0, page_size: int = PAGE_SIZE,
+                  sm_scale: Optional[float] = None) -> Workload:
+    """decodes: list of (o, L) for 32-row block decodes (n = min(32, L - o));
+    prefills: list of L. Pages are drawn from ``rng`` (default: seeded by seed)."""
+    if rng is None:
+        rng = np.random.default_rng(seed)
+    q_off, kv_len, n_rows, pre = [], [], [], []
+    for (o, L) in decodes:
+        q_off.append(o)
+        kv_len.append(L)
+        n_rows.append(min(BLOCK, L - o))
+        pre.append(False)
+    for L in prefills:
+        q_off.append(0)
+        kv_len.append(L)
+        n_rows.append(L)
+        pre.append(True)
+    kv_len_a = np.asarray(kv_len, dtype=np.int32)
+    npages = (kv_len_a.astype(np.int64) + page_size - 1) // page_size
+    needed = int(npages.sum())
+    pool = pool_pages if pool_pages is not None else max(2 * needed, 1)
+    perm = rng.permutation(pool)[:needed].astype(np.int32)
+    page_indptr = np.zeros(len(kv_len) + 1, dtype=np.int32)
+    page_indptr[1:] = np.cumsum(npages)
+    q_indptr = np.zeros(len(kv_len) + 1, dtype=np.int32)
+    q_indptr[1:] = np.cumsum(n_rows)
+    if sm_scale is None:
+        sm_scale = float(np.float32(1.0 / math.sqrt(d)))
+    return Workload(name=name, seed=seed, num_q_heads=hq, num_kv_heads=hkv, head_dim=d,
+                    q_indptr=q_indptr, q_offset=np.asarray(q_off, dtype=np.int32),
+                    kv_len=kv_len_a, is_prefill=np.asarray(pre, dtype=bool),
+                    page_indptr=page_indptr, page_ids=perm, num_pool_pages=pool,
+                    sm_scale=sm_scale, q_scale=q_scale, page_size=page_size)
+
+
+def _decodes_from_prompts(rng, prompts, resp) -> List[Tuple[int, int]]:
+    blocks = rng.integers(0, resp // BLOCK, size=len(prompts))
+    return [(int(P) + BLOCK * int(b), int(P) + resp) for P, b in zip(prompts, blocks)]
+
+
+def tiny_mixed(seed: int = 0) -> Workload:
+    """Single request, one layer: MHA 4/4, D 64, prompt 96 + 32 masked response
+    positions (L = 128). Item 0 is the block decode of rows 96..127 over all 128
+    cached positions; item 1 is the whole 128-token prefill. The decode's cache
+    is the prefill's K/V and its query / fresh K/V rows are the prefill's rows
+    96..127, so decode rows must equal prefill rows 96..127."""
+    w = make_workload("tiny_mixed", seed, hq=4, hkv=4, d=64, decodes=[(96, 128)], prefills=[128])
+    base = Workload(**{f.name: getattr(w, f.name) for f in dataclasses.fields(w)})
+    base.value_fn = None
+
+    def value_fn(item, kind):
+        # everything is drawn as item 1 (the prefill); item 0 views into it
+        if item == 1:
+            return None
+        if kind == KIND_Q:
+            return base.q(1)[96:128].float()
+        if kind == KIND_KNEW:
+            return base.k_new(1)[96:128].float()
+        if kind == KIND_VNEW:
+            return base.v_new(1)[96:128].float()
+        if kind == KIND_KCTX:
+            return base.k_new(1).float()
+        if kind == KIND_VCTX:
+            return base.v_new(1).float()
+        return None
+
+    w.value_fn = value_fn
+    return w
+
+
+def llada_decode(seed: int = 0) -> Workload:
+    """LLaDA-8B-shaped layer, decode only: MHA 32/32, D 128; 32 block decodes,
+    prompts ~ LN(300, 0.8) in [16, 2048] + 256 response, block index 0..7."""
+    rng = np.random.default_rng(seed)
+    P = _lognormal_lengths(rng, 32, 300, 0.8, 16, 2048)
+    dec = _decodes_from_prompts(rng, P, 256)
+    return make_workload("llada_decode", seed, hq=32, hkv=32, d=128, decodes=dec, prefills=[], rng=rng)
+
+
+def dream_mixed(seed: int = 0) -> Workload:
+    """Dream-7B-shaped layer, mixed batch: GQA 28/4, D 128; 48 block decodes
+    (prompts ~ LN(500, 0.8) in [16, 4096] + 256) plus two whole prefills of
+    L = 2304 and 3328."""
+    rng = np.random.default_rng(seed)
+    P = _lognormal_lengths(rng, 48, 500, 0.8, 16, 4096)
+    dec = _decodes_from_prompts(rng, P, 256)
+    return make_workload("dream_mixed", seed, hq=28, hkv=4, d=128, decodes=dec,
+                         prefills=[2304, 3328], rng=rng)
+
+
+def prefill_heavy(seed: int = 0) -> Workload:
+    """Long-document prefills: GQA 28/4, D 128; 8 whole prefills with prompts
+    ~ LN(6000, 0.5) in [1024, 16384] + 256 response; KV written to pages."""
+    rng = np.random.default_rng(seed)
+    P = _lognormal_lengths(rng, 8, 6000, 0.5, 1024, 16384)
+    return make_workload("prefill_heavy", seed, hq=28, hkv=4, d=128, decodes=[],
+                         prefills=[int(p) + 256 for p in P], rng=rng)
+
+
+LONG_DECODE_POOL_PAGES = 262_144  # 64 GiB of K+V pages at MHA 32 heads, D 128
+
+
+def long_decode(seed: int = 0) -> Workload:
+    """High-concurrency long-context decode: MHA 32/32, D 128; 256 block
+    decodes, prompts ~ LN(1200, 1.0) in [16, 32768] + 512 response, block index
+    0..15, pages scattered over a 64 GiB pool (262,144 pages)."""
+    rng = np.random.default_rng(seed)
+    P = _lognormal_lengths(rng, 256, 1200, 1.0, 16, 32768)
+    dec = _decodes_from_prompts(rng, P, 512)
+    return make_workload("long_decode", seed, hq=32, hkv=32, d=128, decodes=dec, prefills=[],
+                         rng=rng, pool_pages=LONG_DECODE_POOL_PAGES)
+
+
+CONFIGS = {
+    0: tiny_mixed,
+    1: llada_decode,
+    2: dream_mixed,
+    3: prefill_heavy,
+    4: long_decode,
+}
+
+
+def by_index(idx: int, seed: int = 0) -> Workload:
+    return CONFIGS[idx](seed)
+
+
+def ragged_small(seed: int, *, hq: int, hkv: int, d: int, q_scale: float = 1.0) -> Workload:
+    """Small ragged mixed batch spanning several tiles and ragged tails: block
+    decodes with partial last pages and short / odd-length prefills."""
+    rng = np.random.default_rng(1000 + seed)
+    dec = []
+    for L in (37, 130, 333, 700, 64, 1025):
+        o = int(rng.integers(0, max(1, L - 8)))
+        dec.append((o, L))
+    pre = [1, 19, 150, 301]
+    return make_workload(f"ragged_small_{hq}_{hkv}_{d}", seed, hq=hq, hkv=hkv, d=d,
+                         decodes=dec, prefills=pre, rng=rng, q_scale=q_scale)
