@@ -1,0 +1,242 @@
+#!/usr/bin/env python3
+"""Benchmark of the mixed block-decode / prefill attention call on one MI355X.
+
+A step is one whole call: KV write-back, the prefill-shaped and the
+decode-shaped attention launches and the split merge, over one batch whose
+inputs are already resident in HBM. Prints one JSON line (rank 0).
+
+    python bench.py [--steps K] [--warmup W] [--workload NAME] [--seed S]
+
+Work counts are algorithmic: F = sum 4 n L D Hq flops (QK^T and PV, no causal
+halving) and B = K/V read once per item + cache write of the fresh rows + Q
+read + O write + page ids + LSE write.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "attention TFLOP/s + KV HBM GB/s (frac. of roofline), mixed decode/prefill batch"
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+PHASES = ("kv_write", "prefill_attn", "decode_attn", "merge")
+
+
+def split_work(wl):
+    """Algorithmic flops / bytes of each launch of the call."""
+    import numpy as np
+    n = np.diff(wl.q_indptr).astype(np.float64)
+    L = wl.kv_len.astype(np.float64)
+    D, Hq, Hkv = wl.head_dim, wl.num_q_heads, wl.num_kv_heads
+    pre = n > 32
+    flops = 4.0 * n * L * D * Hq
+    # attention launch: K/V read once, Q read, O write, LSE write, page ids (decode)
+    attn_b = 2.0 * (2 * L * Hkv * D + 2 * n * Hq * D) + 4.0 * n * Hq
+    attn_b += np.where(pre, 0.0, 4.0 * np.ceil(L / 16))
+    write_b = 2.0 * (2 * n * Hkv * D) * 2  # read k_new/v_new, write them to pages
+    return {
+        "prefill_attn": (float(flops[pre].sum()), float(attn_b[pre].sum())),
+        "decode_attn": (float(flops[~pre].sum()), float(attn_b[~pre].sum())),
+        "kv_write": (0.0, float(write_b.sum())),
+    }
+
+
+def cpu_baseline(wl, budget_s):
+    """Time the oracle on a bounded sample of the same workload."""
+    import numpy as np
+    from oracle import oracle
+    threads = oracle.threads(len(os.sched_getaffinity(0)))
+    D, Hq = wl.head_dim, wl.num_q_heads
+
+    def rows_of(i, cap):
+        n = wl.n(i)
+        return np.arange(n) if n <= cap else np.linspace(0, n - 1, cap).astype(np.int64)
+
+    def flops_of(sel):
+        return sum(4.0 * len(r) * int(wl.kv_len[i]) * D * Hq for i, r in sel.items())
+
+    # calibrate on the first item (a few rows), then fill the budget
+    first = {0: rows_of(0, 8)}
+    t = time.perf_counter()
+    oracle.attention(wl, items=[0], rows=first)
+    rate = flops_of(first) / max(time.perf_counter() - t, 1e-6)
+    target = rate * budget_s
+    sel, acc = {}, 0.0
+    for cap in (32, 64):
+        for i in range(wl.num_items):
+            if i in sel:
+                continue
+            r = rows_of(i, cap)
+            f = 4.0 * len(r) * int(wl.kv_len[i]) * D * Hq
+            if acc + f > target and sel:
+                continue
+            sel[i] = r
+            acc += f
+    t = time.perf_counter()
+    oracle.attention(wl, items=sorted(sel), rows=sel)
+    dt = time.perf_counter() - t
+    n_dec = sum(1 for i in sel if wl.n(i) <= 32)
+    n_pre = len(sel) - n_dec
+    sample = (f"{n_dec} block decodes (all rows, all heads) and {n_pre} prefills "
+              f"(up to 64 evenly spaced rows, all heads) of {wl.name} seed {wl.seed}: "
+              f"{acc / 1e9:.1f} GFLOP in {dt:.1f} s")
+    return {"value": acc / dt / 1e12, "unit": "TFLOP/s", "cores": threads, "kind": "oracle",
+            "sample": sample, "seconds": dt}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="dream_mixed",
+                    choices=["tiny_mixed", "llada_decode", "dream_mixed", "prefill_heavy", "long_decode"])
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle work")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--flush", action="store_true",
+                    help="overwrite 512 MiB between steps (outside the timing) so no step reads "
+                         "the previous one's data from the 256 MB Infinity Cache; steps are then "
+                         "timed by events")
+    args = ap.parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(run with --gpus 1).", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import workloads
+    from paper_2607_04206_amd import attn
+    from paper_2607_04206_amd._lib import check, lib
+
+    dev = torch.device("cuda:0")
+    wl = getattr(workloads, args.workload)(args.seed)
+    print(f"[bench] {wl.name} seed {wl.seed}: drawing inputs", file=sys.stderr, flush=True)
+    t = workloads.device_inputs(wl, dev, fill=None)
+
+    t0 = time.perf_counter()
+    p = attn.plan(q_indptr=wl.q_indptr, q_offset=wl.q_offset, kv_len=wl.kv_len,
+                  page_indptr=wl.page_indptr, page_ids=wl.page_ids, num_q_heads=wl.num_q_heads,
+                  num_kv_heads=wl.num_kv_heads, head_dim=wl.head_dim,
+                  num_pool_pages=wl.num_pool_pages, sm_scale=wl.sm_scale)
+    plan_ms = (time.perf_counter() - t0) * 1e3
+    p.to(dev)
+    T, Hq, D = wl.total_q, wl.num_q_heads, wl.head_dim
+    out = torch.empty((T, Hq, D), dtype=torch.bfloat16, device=dev)
+    lse = torch.empty((T, Hq), dtype=torch.float32, device=dev)
+    ws = torch.empty((max(p.workspace_bytes, 16),), dtype=torch.uint8, device=dev)
+    stream = torch.cuda.current_stream(dev)
+    import ctypes
+    args_c = [p.host_ptr(), p.dev.data_ptr(), t["q"].data_ptr(), t["k_new"].data_ptr(),
+              t["v_new"].data_ptr(), t["k_cache"].data_ptr(), t["v_cache"].data_ptr(),
+              t["page_ids"].data_ptr(), out.data_ptr(), lse.data_ptr(), ws.data_ptr(), ws.numel(),
+              stream.cuda_stream]
+
+    def make_events():
+        evs = [torch.cuda.Event(enable_timing=True) for _ in range(5)]
+        for e in evs:
+            e.record(stream)  # creates the HIP event
+        arr = (ctypes.c_void_p * 5)(*[e.cuda_event for e in evs])
+        return evs, arr
+
+    flush_buf = torch.empty((512 << 20,), dtype=torch.uint8, device=dev) if args.flush else None
+
+    for _ in range(args.warmup):
+        check(lib.sangam_attn_forward(*args_c))
+    torch.cuda.synchronize()
+    print(f"[bench] warmup done ({args.warmup} steps)", file=sys.stderr, flush=True)
+
+    K = args.steps
+    evsets = [make_events() for _ in range(K)]
+    torch.cuda.synchronize()
+    if args.flush:
+        for k in range(K):
+            flush_buf.fill_(k & 0xFF)
+            check(lib.sangam_attn_forward_timed(*args_c, evsets[k][1]))
+        torch.cuda.synchronize()
+        step_ms = [evsets[k][0][0].elapsed_time(evsets[k][0][4]) for k in range(K)]
+        ms_per_step = float(np.mean(step_ms))
+    else:
+        torch.cuda.synchronize()
+        w0 = time.perf_counter()
+        for k in range(K):
+            check(lib.sangam_attn_forward_timed(*args_c, evsets[k][1]))
+        torch.cuda.synchronize()
+        ms_per_step = (time.perf_counter() - w0) * 1e3 / K
+    print(f"[bench] timed {K} steps: {ms_per_step:.4f} ms/step", file=sys.stderr, flush=True)
+
+    phase_ms = {}
+    for j, name in enumerate(PHASES):
+        phase_ms[name] = float(np.mean([evsets[k][0][j].elapsed_time(evsets[k][0][j + 1])
+                                        for k in range(K)]))
+
+    F, B = wl.flops(), wl.hbm_bytes()
+    sec = ms_per_step / 1e3
+    tflops, gbs = F / sec / 1e12, B / sec / 1e9
+    t_star = max(F / (PEAK_BF16_TFLOPS * 1e12), B / (PEAK_HBM_GBS * 1e9))
+
+    work = split_work(wl)
+    dom = max(("prefill_attn", "decode_attn"), key=lambda n: phase_ms[n] if work[n][0] > 0 else -1)
+    f_d, b_d = work[dom]
+    t_d = phase_ms[dom] / 1e3
+    intensity = f_d / max(b_d, 1.0)
+    if intensity >= PEAK_BF16_TFLOPS * 1e12 / (PEAK_HBM_GBS * 1e9):
+        roof = {"bound": "mfma", "achieved": f_d / t_d / 1e12, "peak": PEAK_BF16_TFLOPS,
+                "unit": "TFLOP/s"}
+    else:
+        roof = {"bound": "hbm", "achieved": b_d / t_d / 1e9, "peak": PEAK_HBM_GBS, "unit": "GB/s"}
+    roof["frac"] = roof["achieved"] / roof["peak"]
+    roof["traffic"] = None
+    roof["kernel"] = dom
+    roof["kernel_ms"] = phase_ms[dom]
+    roof["algorithmic_flops"] = f_d
+    roof["algorithmic_bytes"] = b_d
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        print("[bench] timing the oracle on a CPU sample", file=sys.stderr, flush=True)
+        cpu = cpu_baseline(wl, args.cpu_budget)
+
+    n_dec = int((np.diff(wl.q_indptr) <= 32).sum())
+    res = {
+        "metric": METRIC,
+        "value": tflops,
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": wl.name, "seed": wl.seed, "block_decodes": n_dec,
+                   "prefills": wl.num_items - n_dec, "num_q_heads": wl.num_q_heads,
+                   "num_kv_heads": wl.num_kv_heads, "head_dim": wl.head_dim, "page_size": 16,
+                   "query_rows": T, "context_tokens": int(wl.kv_len.sum()),
+                   "parallelism": "1 GPU", "mall_flush": bool(args.flush)},
+        "tflops": tflops,
+        "hbm_gbs": gbs,
+        "mfma_frac": tflops / PEAK_BF16_TFLOPS,
+        "hbm_frac": gbs / PEAK_HBM_GBS,
+        "roofline_frac": t_star / sec,
+        "algorithmic_flops": F,
+        "algorithmic_bytes": B,
+        "phase_ms": phase_ms,
+        "plan_ms": plan_ms,
+        "roofline": roof,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

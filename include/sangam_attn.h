@@ -1,0 +1,166 @@
+/*
+ * sangam_attn.h - C ABI of the mixed block-decode / prefill attention call of
+ * cached diffusion-LLM serving, for AMD Instinct MI355X (gfx950).
+ *
+ * The operation (Sangam paper: Sec. 2.1 bidirectional attention, Sec. 2.2
+ * blockwise approximate KV cache, Sec. 4.1 / Alg. 1 mixed microbatches of
+ * in-flight decodes plus whole prefills, Sec. 5 paged KV cache, Sec. 6.1
+ * page size 16, block size 32, bf16):
+ *
+ *   One call serves a ragged batch of work items. Item i has n_i query rows
+ *   at sequence positions o_i .. o_i+n_i-1 (the block-offset table) and a
+ *   context of L_i positions. A block decode has n_i = 32 rows (one response
+ *   block) and reuses the request's cached KV; a prefill has o_i = 0,
+ *   n_i = L_i and brings its whole sequence. For each item the call
+ *     1. writes the fresh rows k_new / v_new into the paged cache at positions
+ *        [o_i, o_i+n_i), and
+ *     2. lets every query row attend, without a causal mask, to all positions
+ *        [0, L_i) of the item's post-write sequence:
+ *          out[r,h,:] = softmax_j(sm_scale * q[r,h,:] . K[j,g,:]) V[j,g,:]
+ *          lse[r,h]   = ln sum_j exp(sm_scale * q[r,h,:] . K[j,g,:])
+ *        with g = h / (Hq / Hkv) (contiguous GQA groups).
+ *   Attention reads the item's own fresh rows from k_new / v_new, never from
+ *   the cache, so the write and the reads of one launch never race.
+ *
+ * Layouts (row-major, contiguous, 16-byte aligned; bf16 = IEEE bfloat16 bits):
+ *   q, out          [sum n_i, Hq, D]  bf16   (item i's rows start at q_indptr[i])
+ *   k_new, v_new    [sum n_i, Hkv, D] bf16   (row t of item i = position o_i + t)
+ *   k_cache,v_cache [num_pool_pages, Hkv, page_size, D] bf16
+ *                   position p of item i lives in page
+ *                   page_ids[page_indptr[i] + p / page_size], slot p % page_size
+ *   lse             [sum n_i, Hq] fp32 (natural log), may be NULL
+ * Slots >= L_i of an item's last page are never read and never written.
+ *
+ * Ownership: the caller owns every host and device buffer, including the plan
+ * buffer, its device copy and the workspace. The library allocates nothing,
+ * holds no device state and keeps no pointer after a call returns.
+ *
+ * Errors: every entry point returns a sangam_status (0 = success, negative =
+ * failure) and never throws or aborts; sangam_last_error() gives a message
+ * for the calling thread's last failure.
+ */
+#ifndef SANGAM_ATTN_H
+#define SANGAM_ATTN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef int32_t sangam_status;
+
+#define SANGAM_OK 0
+#define SANGAM_ERR_INVALID_ARG (-1) /* malformed descriptor or argument */
+#define SANGAM_ERR_UNSUPPORTED (-2) /* head_dim not 64/128, page_size not 16, Hq % Hkv != 0 */
+#define SANGAM_ERR_PAGE_RANGE (-3)  /* a page id outside [0, num_pool_pages) */
+#define SANGAM_ERR_PAGE_ALIAS (-4)  /* a page listed twice in one batch */
+#define SANGAM_ERR_BUFFER (-5)      /* plan buffer or workspace too small */
+#define SANGAM_ERR_ALIGN (-6)       /* a tensor pointer not 16-byte aligned */
+#define SANGAM_ERR_HIP (-7)         /* a HIP runtime error during launch */
+#define SANGAM_ERR_PLAN (-8)        /* not a plan of this library version */
+
+/* Batch descriptor. All arrays are host memory, read only during the call. */
+typedef struct sangam_attn_desc {
+    int32_t num_items;       /* number of work items, >= 1 */
+    int32_t num_q_heads;     /* Hq >= 1 */
+    int32_t num_kv_heads;    /* Hkv >= 1, Hq % Hkv == 0 */
+    int32_t head_dim;        /* D: 64 or 128 */
+    int32_t page_size;       /* tokens per KV page: 16 */
+    int32_t force_kv_splits; /* 0: the plan chooses; k >= 1: split every item's context
+                                into min(k, ceil(L_i / 64)) chunks (tests, tuning) */
+    int64_t num_pool_pages;  /* pages in k_cache / v_cache */
+    float sm_scale;          /* softmax scale, e.g. 1/sqrt(D) */
+    int32_t num_cus;         /* compute units to balance over; 0 means 256 */
+    const int32_t *q_indptr;    /* [num_items + 1], q_indptr[0] = 0, n_i = q_indptr[i+1]-q_indptr[i] >= 1 */
+    const int32_t *q_offset;    /* [num_items] block-offset table o_i >= 0, o_i + n_i <= L_i */
+    const int32_t *kv_len;      /* [num_items] L_i >= 1 */
+    const int32_t *page_indptr; /* [num_items + 1], page_indptr[i+1]-page_indptr[i] = ceil(L_i/page_size) */
+    const int32_t *page_ids;    /* [page_indptr[num_items]], in range, no page twice */
+} sangam_attn_desc;
+
+/*
+ * Validate a batch and write its launch plan into plan_buf (host memory).
+ * Host only: makes no HIP call. The plan is position independent; the caller
+ * copies the same bytes to device memory (plan_dev below) before the forward.
+ * If cap is too small, returns SANGAM_ERR_BUFFER with *used = bytes needed
+ * (plan_buf may be NULL to query the size). On success *used = bytes written.
+ * Errors: SANGAM_ERR_INVALID_ARG, _UNSUPPORTED, _PAGE_RANGE, _PAGE_ALIAS, _BUFFER.
+ */
+sangam_status sangam_attn_plan(const sangam_attn_desc *desc, void *plan_buf, size_t cap,
+                               size_t *used);
+
+/* Device workspace bytes the forward needs for split-KV partial results
+ * (fp32 O and LSE); 0 when no item is split. Returns 0 for an invalid plan. */
+size_t sangam_plan_workspace_bytes(const void *plan_buf);
+
+/* Summary of a plan, for tests and tuning. */
+typedef struct sangam_plan_info {
+    int32_t num_items;
+    int32_t num_decode_tiles;  /* work-groups of the decode-shaped launch (n_i <= 32) */
+    int32_t num_prefill_tiles; /* work-groups of the prefill-shaped launch (n_i > 32) */
+    int32_t num_split_items;   /* items whose context is split (merged afterwards) */
+    int32_t max_splits;        /* largest split count of an item */
+    int32_t decode_q_waves;    /* waves per decode work-group that hold query rows */
+    int32_t decode_kv_waves;   /* waves per decode work-group that split the context */
+    int32_t reserved;
+    int64_t total_q_rows;      /* sum n_i */
+    int64_t workspace_bytes;
+    int64_t plan_bytes;
+} sangam_plan_info;
+
+sangam_status sangam_plan_get_info(const void *plan_buf, sangam_plan_info *info);
+
+/* Split count and first context position of each split of item `item`.
+ * starts must hold max_splits + 1 entries (the last one is L_i). */
+sangam_status sangam_plan_item_splits(const void *plan_buf, int32_t item, int32_t *num_splits,
+                                      int32_t *starts, int32_t cap);
+
+/*
+ * Run the call on `stream` (a hipStream_t; NULL is the default stream).
+ * Asynchronous: it only enqueues kernels. It allocates nothing, never
+ * synchronizes and copies nothing between host and device, so it may be
+ * captured into a HIP graph. plan_host is the plan in host memory (launch
+ * sizes are read from it); plan_dev is the same bytes in device memory.
+ * page_ids_dev holds desc->page_ids in device memory. lse may be NULL.
+ * workspace must hold sangam_plan_workspace_bytes(plan_host) bytes (NULL
+ * when that is 0); workspace_bytes is its size.
+ * Errors: SANGAM_ERR_PLAN, _INVALID_ARG (a NULL tensor), _ALIGN, _BUFFER
+ * (workspace too small), _HIP (launch failed; nothing is rolled back).
+ */
+sangam_status sangam_attn_forward(const void *plan_host, const void *plan_dev, const void *q,
+                                  const void *k_new, const void *v_new, void *k_cache,
+                                  void *v_cache, const int32_t *page_ids_dev, void *out,
+                                  float *lse, void *workspace, size_t workspace_bytes,
+                                  void *stream);
+
+/*
+ * sangam_attn_forward, plus HIP events recorded on `stream` around its
+ * phases, for measuring each kernel in place: events[0] before the KV
+ * write-back, [1] before the prefill-shaped attention launch, [2] before the
+ * decode-shaped launch, [3] before the split merge, [4] after it. A phase with
+ * no work records its two events back to back. events holds five hipEvent_t
+ * the caller created (and owns); otherwise identical to sangam_attn_forward.
+ * Errors: as sangam_attn_forward, plus SANGAM_ERR_INVALID_ARG for a NULL
+ * event.
+ */
+sangam_status sangam_attn_forward_timed(const void *plan_host, const void *plan_dev,
+                                        const void *q, const void *k_new, const void *v_new,
+                                        void *k_cache, void *v_cache, const int32_t *page_ids_dev,
+                                        void *out, float *lse, void *workspace,
+                                        size_t workspace_bytes, void *stream,
+                                        void *const *events);
+
+/* Message of the calling thread's last failure ("" if none). The pointer
+ * stays valid until the thread's next call into the library. */
+const char *sangam_last_error(void);
+
+/* Library version, e.g. 0x000100 for 0.1.0. */
+int32_t sangam_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SANGAM_ATTN_H */

@@ -1,0 +1,150 @@
+"""Python face of the C ABI: the same two calls, plan and forward, over torch
+tensors. Argument marshalling only: every step of the attention call runs in
+the HIP kernels of libsangam_attn.so; PyTorch supplies device memory and the
+stream."""
+from __future__ import annotations
+
+import ctypes
+from dataclasses import dataclass
+from typing import Optional, Tuple
+
+import numpy as np
+import torch
+
+from . import _lib
+from ._lib import AttnDesc, PlanInfo, SangamError, check, lib
+
+
+def _i32(a) -> np.ndarray:
+    return np.ascontiguousarray(np.asarray(a, dtype=np.int32))
+
+
+@dataclass
+class Plan:
+    host: np.ndarray                 # uint8 blob (host)
+    dev: Optional[torch.Tensor]      # the same bytes on the device (None before upload)
+    info: PlanInfo
+    num_q_heads: int
+    num_kv_heads: int
+    head_dim: int
+    total_q: int
+
+    @property
+    def workspace_bytes(self) -> int:
+        return int(self.info.workspace_bytes)
+
+    def host_ptr(self) -> int:
+        return self.host.ctypes.data
+
+    def item_splits(self, item: int):
+        n = ctypes.c_int32(0)
+        check(lib.sangam_plan_item_splits(self.host_ptr(), item, ctypes.byref(n), None, 0))
+        starts = np.zeros(n.value + 1, np.int32)
+        check(lib.sangam_plan_item_splits(self.host_ptr(), item, ctypes.byref(n),
+                                          starts.ctypes.data, len(starts)))
+        return starts
+
+    def to(self, device) -> "Plan":
+        """Copy the blob to device memory (the caller's H2D copy of plan_dev)."""
+        t = torch.from_numpy(self.host)
+        self.dev = t.to(device)
+        return self
+
+
+def make_desc(*, q_indptr, q_offset, kv_len, page_indptr, page_ids, num_q_heads, num_kv_heads,
+              head_dim, num_pool_pages, sm_scale, page_size=16, force_kv_splits=0, num_cus=0):
+    arrays = [_i32(x) for x in (q_indptr, q_offset, kv_len, page_indptr, page_ids)]
+    d = AttnDesc()
+    d.num_items = int(len(arrays[1]))
+    d.num_q_heads = int(num_q_heads)
+    d.num_kv_heads = int(num_kv_heads)
+    d.head_dim = int(head_dim)
+    d.page_size = int(page_size)
+    d.force_kv_splits = int(force_kv_splits)
+    d.num_pool_pages = int(num_pool_pages)
+    d.sm_scale = float(np.float32(sm_scale))
+    d.num_cus = int(num_cus)
+    d.q_indptr, d.q_offset, d.kv_len, d.page_indptr, d.page_ids = (a.ctypes.data for a in arrays)
+    return d, arrays  # keep arrays alive while d is used
+
+
+def plan(*, q_indptr, q_offset, kv_len, page_indptr, page_ids, num_q_heads, num_kv_heads, head_dim,
+         num_pool_pages, sm_scale, page_size=16, force_kv_splits=0, num_cus=0,
+         device=None) -> Plan:
+    """sangam_attn_plan: validate the batch and build its launch plan (host only).
+    With ``device`` the blob is also copied to that device."""
+    d, keep = make_desc(q_indptr=q_indptr, q_offset=q_offset, kv_len=kv_len,
+                        page_indptr=page_indptr, page_ids=page_ids, num_q_heads=num_q_heads,
+                        num_kv_heads=num_kv_heads, head_dim=head_dim,
+                        num_pool_pages=num_pool_pages, sm_scale=sm_scale, page_size=page_size,
+                        force_kv_splits=force_kv_splits, num_cus=num_cus)
+    used = ctypes.c_size_t(0)
+    st = lib.sangam_attn_plan(ctypes.byref(d), None, 0, ctypes.byref(used))
+    if st not in (_lib.SANGAM_OK, -5):  # -5: buffer too small, *used holds the size
+        check(st)
+    buf = np.zeros(int(used.value), np.uint8)
+    check(lib.sangam_attn_plan(ctypes.byref(d), buf.ctypes.data, buf.nbytes, ctypes.byref(used)))
+    info = PlanInfo()
+    check(lib.sangam_plan_get_info(buf.ctypes.data, ctypes.byref(info)))
+    del keep
+    p = Plan(host=buf, dev=None, info=info, num_q_heads=int(num_q_heads),
+             num_kv_heads=int(num_kv_heads), head_dim=int(head_dim),
+             total_q=int(info.total_q_rows))
+    if device is not None:
+        p.to(device)
+    return p
+
+
+def _need(t: torch.Tensor, name: str, dtype, shape, device):
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} must have shape {tuple(shape)}, got {tuple(t.shape)}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if t.device != device:
+        raise ValueError(f"{name} must be on {device}, got {t.device}")
+
+
+def forward(p: Plan, q: torch.Tensor, k_new: torch.Tensor, v_new: torch.Tensor,
+            k_cache: torch.Tensor, v_cache: torch.Tensor, page_ids: torch.Tensor,
+            out: Optional[torch.Tensor] = None, lse: Optional[torch.Tensor] = None,
+            workspace: Optional[torch.Tensor] = None, want_lse: bool = True,
+            stream: Optional[torch.cuda.Stream] = None) -> Tuple[torch.Tensor, Optional[torch.Tensor]]:
+    """sangam_attn_forward on the current (or given) stream. Allocates out,
+    lse and the workspace with torch when they are not passed."""
+    dev = q.device
+    if dev.type != "cuda":
+        raise ValueError("forward needs device tensors (a ROCm GPU)")
+    T, Hq, Hkv, D = p.total_q, p.num_q_heads, p.num_kv_heads, p.head_dim
+    _need(q, "q", torch.bfloat16, (T, Hq, D), dev)
+    _need(k_new, "k_new", torch.bfloat16, (T, Hkv, D), dev)
+    _need(v_new, "v_new", torch.bfloat16, (T, Hkv, D), dev)
+    _need(k_cache, "k_cache", torch.bfloat16, None, dev)
+    _need(v_cache, "v_cache", torch.bfloat16, tuple(k_cache.shape), dev)
+    if k_cache.dim() != 4 or k_cache.shape[1] != Hkv or k_cache.shape[2] != 16 or k_cache.shape[3] != D:
+        raise ValueError("k_cache must be [num_pool_pages, Hkv, 16, D]")
+    _need(page_ids, "page_ids", torch.int32, None, dev)
+    if p.dev is None or p.dev.device != dev:
+        p.to(dev)
+    if out is None:
+        out = torch.empty((T, Hq, D), dtype=torch.bfloat16, device=dev)
+    _need(out, "out", torch.bfloat16, (T, Hq, D), dev)
+    if lse is None and want_lse:
+        lse = torch.empty((T, Hq), dtype=torch.float32, device=dev)
+    if lse is not None:
+        _need(lse, "lse", torch.float32, (T, Hq), dev)
+    wsb = p.workspace_bytes
+    if wsb > 0 and workspace is None:
+        workspace = torch.empty((wsb,), dtype=torch.uint8, device=dev)
+    ws_ptr = workspace.data_ptr() if workspace is not None else None
+    ws_len = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    s = stream if stream is not None else torch.cuda.current_stream(dev)
+    check(lib.sangam_attn_forward(p.host_ptr(), p.dev.data_ptr(), q.data_ptr(), k_new.data_ptr(),
+                                  v_new.data_ptr(), k_cache.data_ptr(), v_cache.data_ptr(),
+                                  page_ids.data_ptr(), out.data_ptr(),
+                                  lse.data_ptr() if lse is not None else None, ws_ptr, ws_len,
+                                  s.cuda_stream))
+    return out, lse

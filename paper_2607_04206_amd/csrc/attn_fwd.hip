@@ -1,0 +1,590 @@
+// gfx950 kernels of the mixed block-decode / prefill attention call and the
+// C-ABI forward entry point that launches them.
+//
+// What is computed (Sangam paper, Sec. 2.1 and Sec. 2.2): dLLM attention is
+// bidirectional, so each query row of an item attends to all L positions of
+// its sequence; a block decode recomputes only its 32 block rows and reuses
+// the request's approximately cached KV for every other position, a prefill
+// brings (and writes back) its whole sequence. Batches mix both kinds
+// (Sec. 4.1, Alg. 1); the KV cache is paged with 16-token pages (Sec. 5,
+// Sec. 6.1).
+//
+// Kernels:
+//   kv_write_kernel   scatters k_new / v_new rows into their cache pages.
+//   attn_tiles_kernel one work-group per plan tile: a context range of one
+//                     item and KV head against up to 8 x 32 query rows.
+//                     Per wave: S^T = K Q^T with v_mfma_f32_32x32x16_bf16
+//                     (each lane holds the scores of one query, so row max /
+//                     row sum need one cross-half exchange), online softmax
+//                     in the exp2 domain, P^T rounded to bf16 feeds
+//                     O^T += V^T P^T directly from the score registers.
+//                     K/V stream global -> LDS with global_load_lds_dwordx4
+//                     into XOR-swizzled tiles (double buffered); V^T operands
+//                     come from ds_read_b64_tr_b16 transposing reads.
+//   merge_kernel      combines split-context partial (O, LSE) in split order.
+#include <hip/hip_runtime.h>
+
+#include <string>
+
+#include "../../include/sangam_attn.h"
+#include "plan_format.h"
+
+namespace sangam {
+void set_error(const std::string& msg);
+void clear_error();
+const PlanHeader* check_plan(const void* plan);
+}  // namespace sangam
+
+using namespace sangam;
+
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+#define LDS __attribute__((address_space(3)))
+
+struct AttnArgs {
+    const TileRec* tiles;
+    const ItemRec* items;
+    const int32_t* page_ids;
+    const uint16_t* q;
+    const uint16_t* k_new;
+    const uint16_t* v_new;
+    const uint16_t* k_cache;
+    const uint16_t* v_cache;
+    uint16_t* out;
+    float* lse;
+    float* ws;
+    int32_t hq;
+    int32_t hkv;
+    float scale_log2;
+};
+
+__device__ __forceinline__ int uniform(int x) { return __builtin_amdgcn_readfirstlane(x); }
+
+// Swizzle of 16-byte chunks inside a staged key row. K rows are read one key
+// per lane (ds_read_b128), so consecutive keys rotate their chunks. V rows are
+// read four keys at a time by ds_read_b64_tr_b16, so groups of four keys
+// spread over the LDS banks.
+template <int D>
+__device__ __forceinline__ int swz_k(int r) {
+    return r & (D / 8 - 1);
+}
+template <int D>
+__device__ __forceinline__ int swz_v(int r) {
+    return D == 128 ? ((r & 3) << 2) : (((r >> 1) & 1) << 2);
+}
+
+__device__ __forceinline__ float bf16_bits_to_float(uint16_t b) {
+    return __uint_as_float(uint32_t(b) << 16);
+}
+
+template <int D, int QW, int KW, int NB, bool HEADS_ACROSS>
+__global__ __launch_bounds__(64 * QW * KW) void attn_tiles_kernel(AttnArgs a) {
+    constexpr int NT = 64 * QW * KW;     // threads
+    constexpr int KT = 32 * NB;          // keys per wave per stage
+    constexpr int STEP = KT * KW;        // keys per stage
+    constexpr int NC = D / 8;            // 16-byte chunks per key row
+    constexpr int ROWB = D * 2;          // bytes per key row
+    constexpr int TILE = STEP * ROWB;    // bytes of one staged K (or V) tile
+    constexpr int NCH = STEP * NC;       // 16-byte chunks of one staged tile
+    constexpr int NJ = (NCH + NT - 1) / NT;  // chunk rounds per thread
+    constexpr int DS = D / 16;           // k-steps of the QK^T contraction
+    constexpr int MB = D / 32;           // 32-dim blocks of O^T
+    static_assert(NCH % 64 == 0, "a wave moves whole 1 KiB rows of chunks");
+    constexpr int MERGE_REGS = MB * 16 + 2;
+    static_assert(KW == 1 || (QW * (KW - 1) * MERGE_REGS * 64 * 4) <= 4 * TILE,
+                  "cross-wave merge must fit in the stage buffers");
+
+    __shared__ __attribute__((aligned(1024))) uint8_t smem[4 * TILE];
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = uniform(tid >> 6);
+    const int qs = wave % QW;
+    const int ks = wave / QW;
+    const int qn = lane & 31;   // query (column) this lane holds
+    const int hh = lane >> 5;   // half-wave
+
+    const TileRec t = a.tiles[blockIdx.x];
+    const ItemRec it = a.items[t.item];
+    const int head = HEADS_ACROSS ? t.q_head0 + qs : t.q_head0;
+    const int row = (HEADS_ACROSS ? t.row0 : t.row0 + 32 * qs) + qn;
+    const bool row_ok = row < it.n;
+
+    // ---- Q fragments (B operand: k = dims, n = query), zero for rows past n
+    bf16x8 qf[DS];
+    {
+        const uint16_t* qp = a.q + ((size_t)(it.q_start + (row_ok ? row : 0)) * a.hq + head) * D;
+#pragma unroll
+        for (int s = 0; s < DS; ++s) {
+            u32x4 v = *(const u32x4*)(qp + 16 * s + 8 * hh);
+            if (!row_ok) v = u32x4{0, 0, 0, 0};
+            qf[s] = __builtin_bit_cast(bf16x8, v);
+        }
+    }
+
+    const int kv_begin = t.kv_begin, kv_end = t.kv_end;
+    const int nstages = (kv_end - kv_begin + STEP - 1) / STEP;
+
+    // ---- stage loader: every thread moves NJ 16-byte chunks of K and of V
+    auto issue_stage = [&](int st, int buf) {
+        uint8_t* kb = smem + buf * 2 * TILE;
+        uint8_t* vb = kb + TILE;
+        const int key0 = kv_begin + st * STEP;
+#pragma unroll
+        for (int j = 0; j < NJ; ++j) {
+            if ((NCH % NT) != 0 && j * NT + wave * 64 >= NCH) break;  // wave-uniform
+            const int P = j * NT + tid;
+            const int r = P / NC;
+            const int pos = P % NC;
+            int p = key0 + r;
+            p = p < kv_end ? p : kv_begin;  // past the range: a valid row, masked later
+            const unsigned rel = unsigned(p - it.o);
+            size_t off;
+            const uint16_t *kbase, *vbase;
+            if (rel < unsigned(it.n)) {
+                off = ((size_t)(it.q_start + rel) * a.hkv + t.kv_head) * D;
+                kbase = a.k_new;
+                vbase = a.v_new;
+            } else {
+                const int page = a.page_ids[it.page_start + (p >> 4)];
+                off = (((size_t)page * a.hkv + t.kv_head) * 16 + (p & 15)) * D;
+                kbase = a.k_cache;
+                vbase = a.v_cache;
+            }
+            const int ck = pos ^ swz_k<D>(r);
+            const int cv = pos ^ swz_v<D>(r);
+            const int dst = (j * NT + wave * 64) * 16;
+            __builtin_amdgcn_global_load_lds(kbase + off + ck * 8, (LDS void*)(kb + dst), 16, 0, 0);
+            __builtin_amdgcn_global_load_lds(vbase + off + cv * 8, (LDS void*)(vb + dst), 16, 0, 0);
+        }
+    };
+
+    f32x16 o[MB];
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) o[mb][i] = 0.0f;
+    float m_run = -INFINITY;  // running max (log2 domain) of this lane's query
+    float l_run = 0.0f;       // running sum over this lane's half of the keys
+
+    issue_stage(0, 0);
+    for (int st = 0; st < nstages; ++st) {
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        __syncthreads();
+        if (st + 1 < nstages) issue_stage(st + 1, (st + 1) & 1);
+
+        const uint8_t* kb = smem + (st & 1) * 2 * TILE;
+        const uint8_t* vb = kb + TILE;
+        const int sub0 = ks * KT;                         // wave's first key in the stage
+        const int key0 = kv_begin + st * STEP + sub0;     // its context position
+
+        // S^T = K Q^T: rows = keys, columns = queries
+        f32x16 s[NB];
+#pragma unroll
+        for (int b = 0; b < NB; ++b) {
+#pragma unroll
+            for (int i = 0; i < 16; ++i) s[b][i] = 0.0f;
+            const int r = sub0 + b * 32 + qn;
+#pragma unroll
+            for (int k = 0; k < DS; ++k) {
+                const int c = 2 * k + hh;
+                const bf16x8 kf = *(const LDS bf16x8*)(kb + r * ROWB + ((c ^ swz_k<D>(r)) << 4));
+                s[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[k], s[b], 0, 0, 0);
+            }
+        }
+
+        // online softmax (exp2 domain); keys past the range get -inf
+        float mx = -INFINITY;
+#pragma unroll
+        for (int b = 0; b < NB; ++b)
+#pragma unroll
+            for (int i = 0; i < 16; ++i) {
+                const int key = key0 + b * 32 + 8 * (i >> 2) + 4 * hh + (i & 3);
+                const float v = key < kv_end ? s[b][i] * a.scale_log2 : -INFINITY;
+                s[b][i] = v;
+                mx = fmaxf(mx, v);
+            }
+        mx = fmaxf(mx, __shfl_xor(mx, 32));
+        const float m_new = fmaxf(m_run, mx);
+        const float m_ref = m_new == -INFINITY ? 0.0f : m_new;
+        const float alpha = __builtin_amdgcn_exp2f(m_run - m_ref);
+        m_run = m_new;
+        l_run *= alpha;
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+            for (int i = 0; i < 16; ++i) o[mb][i] *= alpha;
+
+        bf16x8 pf[NB][2];
+#pragma unroll
+        for (int b = 0; b < NB; ++b)
+#pragma unroll
+            for (int i = 0; i < 16; ++i) {
+                const __bf16 pb = (__bf16)__builtin_amdgcn_exp2f(s[b][i] - m_ref);
+                l_run += (float)pb;
+                pf[b][i >> 3][i & 7] = pb;
+            }
+
+        // O^T += V^T P^T; lane slot j of P^T holds key 16kk + 8(j/4) + 4hh + j%4
+        const int g16 = lane >> 4;
+        const int r4 = (lane >> 2) & 3;
+        const int j4 = lane & 3;
+#pragma unroll
+        for (int b = 0; b < NB; ++b)
+#pragma unroll
+            for (int kk = 0; kk < 2; ++kk) {
+                const int ra = sub0 + b * 32 + kk * 16 + 4 * hh + r4;
+                const int rb = ra + 8;
+#pragma unroll
+                for (int mb = 0; mb < MB; ++mb) {
+                    const int dim = mb * 32 + (g16 & 1) * 16 + 4 * j4;
+                    const int cb = dim >> 3;
+                    const int hb = (dim & 7) * 2;
+                    const bf16x4 va = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
+                        (LDS bf16x4*)(vb + ra * ROWB + ((cb ^ swz_v<D>(ra)) << 4) + hb));
+                    const bf16x4 vbv = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
+                        (LDS bf16x4*)(vb + rb * ROWB + ((cb ^ swz_v<D>(rb)) << 4) + hb));
+                    const bf16x8 vf = {va[0], va[1], va[2], va[3], vbv[0], vbv[1], vbv[2], vbv[3]};
+                    o[mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[b][kk], o[mb], 0, 0, 0);
+                }
+            }
+    }
+
+    // ---- combine the context sub-ranges of the waves that share query rows
+    if constexpr (KW > 1) {
+        __syncthreads();
+        float* mbuf = reinterpret_cast<float*>(smem);
+        if (ks > 0) {
+            float* dst = mbuf + (size_t)((qs * (KW - 1) + (ks - 1)) * MERGE_REGS) * 64;
+#pragma unroll
+            for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+                for (int i = 0; i < 16; ++i) dst[(mb * 16 + i) * 64 + lane] = o[mb][i];
+            dst[(MB * 16) * 64 + lane] = m_run;
+            dst[(MB * 16 + 1) * 64 + lane] = l_run;
+        }
+        __syncthreads();
+        if (ks > 0) return;
+        float m_tot = m_run;
+#pragma unroll
+        for (int k = 1; k < KW; ++k) {
+            const float* src = mbuf + (size_t)((qs * (KW - 1) + (k - 1)) * MERGE_REGS) * 64;
+            m_tot = fmaxf(m_tot, src[(MB * 16) * 64 + lane]);
+        }
+        const float sc0 = __builtin_amdgcn_exp2f(m_run - m_tot);
+        l_run *= sc0;
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+            for (int i = 0; i < 16; ++i) o[mb][i] *= sc0;
+#pragma unroll
+        for (int k = 1; k < KW; ++k) {
+            const float* src = mbuf + (size_t)((qs * (KW - 1) + (k - 1)) * MERGE_REGS) * 64;
+            const float sck = __builtin_amdgcn_exp2f(src[(MB * 16) * 64 + lane] - m_tot);
+            l_run += sck * src[(MB * 16 + 1) * 64 + lane];
+#pragma unroll
+            for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+                for (int i = 0; i < 16; ++i) o[mb][i] += sck * src[(mb * 16 + i) * 64 + lane];
+        }
+        m_run = m_tot;
+    }
+
+    // ---- epilogue
+    const float l_tot = l_run + __shfl_xor(l_run, 32);
+    const float inv = 1.0f / l_tot;
+    const float lse_val = m_run * 0.69314718055994530942f + logf(l_tot);
+    if (!row_ok) return;
+    if (it.num_splits > 1) {
+        const size_t prow = (size_t)(t.split * it.n + row) * a.hq + head;
+        float* po = a.ws + it.ws_o + prow * D;
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+            for (int q4 = 0; q4 < 4; ++q4) {
+                const int dim = mb * 32 + 8 * q4 + 4 * hh;
+                float4 v = {o[mb][4 * q4] * inv, o[mb][4 * q4 + 1] * inv, o[mb][4 * q4 + 2] * inv,
+                            o[mb][4 * q4 + 3] * inv};
+                *(float4*)(po + dim) = v;
+            }
+        if (hh == 0) a.ws[it.ws_lse + prow] = lse_val;
+    } else {
+        uint16_t* op = a.out + ((size_t)(it.q_start + row) * a.hq + head) * D;
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+            for (int q4 = 0; q4 < 4; ++q4) {
+                const int dim = mb * 32 + 8 * q4 + 4 * hh;
+                const bf16x4 v = {(__bf16)(o[mb][4 * q4] * inv), (__bf16)(o[mb][4 * q4 + 1] * inv),
+                                  (__bf16)(o[mb][4 * q4 + 2] * inv), (__bf16)(o[mb][4 * q4 + 3] * inv)};
+                *(u32x2*)(op + dim) = __builtin_bit_cast(u32x2, v);
+            }
+        if (hh == 0 && a.lse) a.lse[(size_t)(it.q_start + row) * a.hq + head] = lse_val;
+    }
+}
+
+// ---------------------------------------------------------------- KV write
+struct WriteArgs {
+    const ItemRec* items;
+    const int32_t* page_ids;
+    const uint16_t* k_new;
+    const uint16_t* v_new;
+    uint16_t* k_cache;
+    uint16_t* v_cache;
+    int32_t n_items;
+    int32_t hkv;
+    int32_t d;
+    int64_t total_chunks;  // total_q * hkv * d / 8
+};
+
+__global__ __launch_bounds__(256) void kv_write_kernel(WriteArgs a) {
+    const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (idx >= a.total_chunks) return;
+    const int cpr = a.d / 8;
+    const int64_t row = idx / (a.hkv * cpr);
+    const int rem = int(idx - row * a.hkv * cpr);
+    const int g = rem / cpr;
+    const int c = rem - g * cpr;
+    int lo = 0, hi = a.n_items - 1;
+    while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (a.items[mid].q_start <= row) lo = mid;
+        else hi = mid - 1;
+    }
+    const ItemRec& it = a.items[lo];
+    const int p = it.o + int(row - it.q_start);
+    const int page = a.page_ids[it.page_start + (p >> 4)];
+    const size_t dst = (((size_t)page * a.hkv + g) * 16 + (p & 15)) * a.d + c * 8;
+    const size_t src = ((size_t)row * a.hkv + g) * a.d + c * 8;
+    *(u32x4*)(a.k_cache + dst) = *(const u32x4*)(a.k_new + src);
+    *(u32x4*)(a.v_cache + dst) = *(const u32x4*)(a.v_new + src);
+}
+
+// --------------------------------------------------------------- split merge
+struct MergeArgs {
+    const MergeRow* rows;
+    const ItemRec* items;
+    const float* ws;
+    uint16_t* out;
+    float* lse;
+    int32_t hq;
+    int32_t d;
+};
+
+__global__ __launch_bounds__(256) void merge_kernel(MergeArgs a) {
+    const MergeRow mr = a.rows[blockIdx.x];
+    const ItemRec it = a.items[mr.item];
+    const int S = it.num_splits;
+    const int d4n = a.d / 4;
+    for (int e = threadIdx.x; e < a.hq * d4n; e += 256) {
+        const int head = e / d4n;
+        const int d4 = e - head * d4n;
+        float mx = -INFINITY;
+        for (int s = 0; s < S; ++s)
+            mx = fmaxf(mx, a.ws[it.ws_lse + (size_t)(s * it.n + mr.row) * a.hq + head]);
+        float tot = 0.0f;
+        float4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
+        for (int s = 0; s < S; ++s) {
+            const size_t prow = (size_t)(s * it.n + mr.row) * a.hq + head;
+            const float w = __expf(a.ws[it.ws_lse + prow] - mx);
+            const float4 v = *(const float4*)(a.ws + it.ws_o + prow * a.d + 4 * d4);
+            tot += w;
+            acc.x += w * v.x;
+            acc.y += w * v.y;
+            acc.z += w * v.z;
+            acc.w += w * v.w;
+        }
+        const float inv = 1.0f / tot;
+        const bf16x4 v = {(__bf16)(acc.x * inv), (__bf16)(acc.y * inv), (__bf16)(acc.z * inv),
+                          (__bf16)(acc.w * inv)};
+        const size_t orow = (size_t)(it.q_start + mr.row) * a.hq + head;
+        *(u32x2*)(a.out + orow * a.d + 4 * d4) = __builtin_bit_cast(u32x2, v);
+        if (d4 == 0 && a.lse) a.lse[orow] = mx + logf(tot);
+    }
+}
+
+// ------------------------------------------------------------------ launch
+template <int D, int QW, int KW, int NB, bool HA>
+hipError_t launch_tiles(const AttnArgs& args, int n_tiles, hipStream_t stream) {
+    attn_tiles_kernel<D, QW, KW, NB, HA><<<dim3(n_tiles), dim3(64 * QW * KW), 0, stream>>>(args);
+    return hipGetLastError();
+}
+
+template <int D>
+hipError_t launch_decode(const AttnArgs& args, int n_tiles, int qw, int kw, int nb, hipStream_t stream,
+                         bool* supported) {
+    *supported = true;
+    if (qw == 1 && kw == 4 && nb == 1) return launch_tiles<D, 1, 4, 1, true>(args, n_tiles, stream);
+    if (qw == 2 && kw == 2 && nb == 2) return launch_tiles<D, 2, 2, 2, true>(args, n_tiles, stream);
+    if (kw == 1 && nb == 2) {
+        switch (qw) {
+            case 3: return launch_tiles<D, 3, 1, 2, true>(args, n_tiles, stream);
+            case 4: return launch_tiles<D, 4, 1, 2, true>(args, n_tiles, stream);
+            case 5: return launch_tiles<D, 5, 1, 2, true>(args, n_tiles, stream);
+            case 6: return launch_tiles<D, 6, 1, 2, true>(args, n_tiles, stream);
+            case 7: return launch_tiles<D, 7, 1, 2, true>(args, n_tiles, stream);
+            case 8: return launch_tiles<D, 8, 1, 2, true>(args, n_tiles, stream);
+            default: break;
+        }
+    }
+    *supported = false;
+    return hipSuccess;
+}
+
+sangam_status hip_fail(hipError_t e, const char* what) {
+    set_error(std::string(what) + ": " + hipGetErrorString(e));
+    return SANGAM_ERR_HIP;
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+}  // namespace
+
+static sangam_status forward_impl(const void* plan_host, const void* plan_dev, const void* q,
+                                  const void* k_new, const void* v_new, void* k_cache, void* v_cache,
+                                  const int32_t* page_ids_dev, void* out, float* lse, void* workspace,
+                                  size_t workspace_bytes, void* stream_ptr, void* const* events) {
+    clear_error();
+    const PlanHeader* h = check_plan(plan_host);
+    if (!h) {
+        set_error("plan_host is not a plan of this library version");
+        return SANGAM_ERR_PLAN;
+    }
+    if (!plan_dev || !q || !k_new || !v_new || !k_cache || !v_cache || !page_ids_dev || !out) {
+        set_error("plan_dev, q, k_new, v_new, k_cache, v_cache, page_ids_dev and out must not be NULL");
+        return SANGAM_ERR_INVALID_ARG;
+    }
+    if (!aligned16(plan_dev) || !aligned16(q) || !aligned16(k_new) || !aligned16(v_new) ||
+        !aligned16(k_cache) || !aligned16(v_cache) || !aligned16(out) ||
+        (reinterpret_cast<uintptr_t>(page_ids_dev) & 3u) || (lse && (reinterpret_cast<uintptr_t>(lse) & 3u))) {
+        set_error("tensors must be 16-byte aligned (page_ids and lse 4-byte aligned)");
+        return SANGAM_ERR_ALIGN;
+    }
+    if (h->workspace_bytes > 0) {
+        if (!workspace || workspace_bytes < size_t(h->workspace_bytes)) {
+            set_error("workspace needs " + std::to_string(h->workspace_bytes) + " bytes");
+            return SANGAM_ERR_BUFFER;
+        }
+        if (!aligned16(workspace)) {
+            set_error("workspace must be 16-byte aligned");
+            return SANGAM_ERR_ALIGN;
+        }
+    }
+    hipStream_t stream = static_cast<hipStream_t>(stream_ptr);
+    const uint8_t* pd = static_cast<const uint8_t*>(plan_dev);
+    auto mark = [&](int k) -> hipError_t {
+        return events ? hipEventRecord(static_cast<hipEvent_t>(events[k]), stream) : hipSuccess;
+    };
+    if (hipError_t e = mark(0); e != hipSuccess) return hip_fail(e, "event record");
+    const ItemRec* items = reinterpret_cast<const ItemRec*>(pd + h->off_items);
+
+    // 1. write the fresh rows into their pages
+    if (h->total_q > 0) {
+        WriteArgs w{items,
+                    page_ids_dev,
+                    static_cast<const uint16_t*>(k_new),
+                    static_cast<const uint16_t*>(v_new),
+                    static_cast<uint16_t*>(k_cache),
+                    static_cast<uint16_t*>(v_cache),
+                    h->num_items,
+                    h->hkv,
+                    h->d,
+                    h->total_q * h->hkv * (h->d / 8)};
+        const int64_t blocks = (w.total_chunks + 255) / 256;
+        kv_write_kernel<<<dim3(unsigned(blocks)), dim3(256), 0, stream>>>(w);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return hip_fail(e, "kv write launch");
+    }
+    if (hipError_t e = mark(1); e != hipSuccess) return hip_fail(e, "event record");
+
+    AttnArgs args{nullptr,
+                  items,
+                  page_ids_dev,
+                  static_cast<const uint16_t*>(q),
+                  static_cast<const uint16_t*>(k_new),
+                  static_cast<const uint16_t*>(v_new),
+                  static_cast<const uint16_t*>(k_cache),
+                  static_cast<const uint16_t*>(v_cache),
+                  static_cast<uint16_t*>(out),
+                  lse,
+                  static_cast<float*>(workspace),
+                  h->hq,
+                  h->hkv,
+                  h->scale_log2};
+
+    // 2. prefill-shaped tiles (compute-bound) first, then decode-shaped tiles
+    if (h->n_prefill_tiles > 0) {
+        args.tiles = reinterpret_cast<const TileRec*>(pd + h->off_prefill_tiles);
+        hipError_t e = h->d == 128
+                           ? launch_tiles<128, kPrefillQWaves, 1, 2, false>(args, h->n_prefill_tiles, stream)
+                           : launch_tiles<64, kPrefillQWaves, 1, 2, false>(args, h->n_prefill_tiles, stream);
+        if (e != hipSuccess) return hip_fail(e, "prefill attention launch");
+    }
+    if (hipError_t e = mark(2); e != hipSuccess) return hip_fail(e, "event record");
+    if (h->n_decode_tiles > 0) {
+        args.tiles = reinterpret_cast<const TileRec*>(pd + h->off_decode_tiles);
+        bool ok = false;
+        hipError_t e = h->d == 128 ? launch_decode<128>(args, h->n_decode_tiles, h->decode_qw, h->decode_kw,
+                                                        h->decode_nb, stream, &ok)
+                                   : launch_decode<64>(args, h->n_decode_tiles, h->decode_qw, h->decode_kw,
+                                                       h->decode_nb, stream, &ok);
+        if (!ok) {
+            set_error("no decode kernel for this head grouping");
+            return SANGAM_ERR_UNSUPPORTED;
+        }
+        if (e != hipSuccess) return hip_fail(e, "decode attention launch");
+    }
+    if (hipError_t e = mark(3); e != hipSuccess) return hip_fail(e, "event record");
+
+    // 3. merge split contexts
+    if (h->n_merge_rows > 0) {
+        MergeArgs m{reinterpret_cast<const MergeRow*>(pd + h->off_merge),
+                    items,
+                    static_cast<const float*>(workspace),
+                    static_cast<uint16_t*>(out),
+                    lse,
+                    h->hq,
+                    h->d};
+        merge_kernel<<<dim3(unsigned(h->n_merge_rows)), dim3(256), 0, stream>>>(m);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return hip_fail(e, "merge launch");
+    }
+    if (hipError_t e = mark(4); e != hipSuccess) return hip_fail(e, "event record");
+    return SANGAM_OK;
+}
+
+extern "C" sangam_status sangam_attn_forward(const void* plan_host, const void* plan_dev, const void* q,
+                                             const void* k_new, const void* v_new, void* k_cache,
+                                             void* v_cache, const int32_t* page_ids_dev, void* out,
+                                             float* lse, void* workspace, size_t workspace_bytes,
+                                             void* stream) {
+    clear_error();
+    return forward_impl(plan_host, plan_dev, q, k_new, v_new, k_cache, v_cache, page_ids_dev, out, lse,
+                        workspace, workspace_bytes, stream, nullptr);
+}
+
+extern "C" sangam_status sangam_attn_forward_timed(const void* plan_host, const void* plan_dev,
+                                                   const void* q, const void* k_new, const void* v_new,
+                                                   void* k_cache, void* v_cache,
+                                                   const int32_t* page_ids_dev, void* out, float* lse,
+                                                   void* workspace, size_t workspace_bytes, void* stream,
+                                                   void* const* events) {
+    clear_error();
+    if (!events) {
+        set_error("events must not be NULL");
+        return SANGAM_ERR_INVALID_ARG;
+    }
+    for (int k = 0; k < 5; ++k)
+        if (!events[k]) {
+            set_error("events must hold five HIP events");
+            return SANGAM_ERR_INVALID_ARG;
+        }
+    return forward_impl(plan_host, plan_dev, q, k_new, v_new, k_cache, v_cache, page_ids_dev, out, lse,
+                        workspace, workspace_bytes, stream, events);
+}

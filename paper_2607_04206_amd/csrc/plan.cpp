@@ -1,0 +1,336 @@
+// Host-side planner of the mixed block-decode / prefill attention call.
+//
+// Host only: no HIP call is made here, so every descriptor check runs (and is
+// testable) on a CPU. The planner validates the batch, cuts it into
+// work-groups for the two launch shapes, splits long contexts, orders the
+// work-groups longest first and sizes the split-KV workspace.
+//
+// Work-group shapes (the kernels in attn_fwd.hip hold the matching templates):
+//   decode-shaped  (n_i <= 32, a block decode): one work-group per (item, KV
+//                  head, context chunk); each wave holds the 32 block rows of
+//                  one query head of the GQA group, so every K/V tile staged
+//                  in LDS serves the whole group. With few query heads per
+//                  group, extra waves split the chunk further.
+//   prefill-shaped (n_i > 32, a whole prefill): one work-group per (item,
+//                  query head, 128-row block); four waves of 32 rows share
+//                  each staged K/V tile.
+#include <algorithm>
+#include <cstring>
+#include <numeric>
+#include <string>
+#include <vector>
+
+#include "../../include/sangam_attn.h"
+#include "plan_format.h"
+
+namespace sangam {
+
+static thread_local std::string g_last_error;
+
+void set_error(const std::string& msg) { g_last_error = msg; }
+void clear_error() { g_last_error.clear(); }
+
+static sangam_status fail(sangam_status code, const std::string& msg) {
+    set_error(msg);
+    return code;
+}
+
+static inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+static inline int64_t round_up(int64_t a, int64_t b) { return ceil_div(a, b) * b; }
+static inline uint64_t align256(uint64_t x) { return (x + 255u) & ~uint64_t(255); }
+
+// Query heads per decode work-group: the whole GQA group when it fits in
+// eight waves, else the largest divisor of the group that does.
+static int decode_q_waves(int group) {
+    if (group <= 8) return group;
+    for (int w = 8; w >= 1; --w)
+        if (group % w == 0) return w;
+    return 1;
+}
+
+// Context sub-range waves: keep at least four waves per work-group so that
+// enough loads are in flight per CU on the bandwidth-bound decode path.
+static int decode_kv_waves(int qw) {
+    if (qw == 1) return 4;
+    if (qw == 2) return 2;
+    return 1;
+}
+
+const PlanHeader* check_plan(const void* plan) {
+    if (!plan) return nullptr;
+    const PlanHeader* h = static_cast<const PlanHeader*>(plan);
+    if (h->magic != kPlanMagic || h->version != kPlanVersion) return nullptr;
+    return h;
+}
+
+}  // namespace sangam
+
+using namespace sangam;
+
+extern "C" const char* sangam_last_error(void) { return g_last_error.c_str(); }
+
+extern "C" int32_t sangam_version(void) { return 0x000100; }
+
+extern "C" sangam_status sangam_attn_plan(const sangam_attn_desc* d, void* plan_buf, size_t cap,
+                                          size_t* used) {
+    clear_error();
+    if (!d || !used) return fail(SANGAM_ERR_INVALID_ARG, "desc and used must not be NULL");
+    *used = 0;
+    const int n_items = d->num_items;
+    if (n_items < 1) return fail(SANGAM_ERR_INVALID_ARG, "num_items must be >= 1");
+    if (!d->q_indptr || !d->q_offset || !d->kv_len || !d->page_indptr || !d->page_ids)
+        return fail(SANGAM_ERR_INVALID_ARG, "descriptor arrays must not be NULL");
+    if (d->num_q_heads < 1 || d->num_kv_heads < 1)
+        return fail(SANGAM_ERR_INVALID_ARG, "head counts must be >= 1");
+    if (d->num_q_heads % d->num_kv_heads != 0)
+        return fail(SANGAM_ERR_UNSUPPORTED, "num_q_heads must be a multiple of num_kv_heads");
+    if (d->head_dim != 64 && d->head_dim != 128)
+        return fail(SANGAM_ERR_UNSUPPORTED, "head_dim must be 64 or 128");
+    if (d->page_size != 16) return fail(SANGAM_ERR_UNSUPPORTED, "page_size must be 16");
+    if (d->num_pool_pages < 1 || d->num_pool_pages > INT32_MAX)
+        return fail(SANGAM_ERR_INVALID_ARG, "num_pool_pages must be in [1, 2^31)");
+    if (!(d->sm_scale > 0.0f) || d->sm_scale != d->sm_scale || d->sm_scale > 1e30f)
+        return fail(SANGAM_ERR_INVALID_ARG, "sm_scale must be a positive finite number");
+    if (d->force_kv_splits < 0) return fail(SANGAM_ERR_INVALID_ARG, "force_kv_splits must be >= 0");
+    if (d->num_cus < 0) return fail(SANGAM_ERR_INVALID_ARG, "num_cus must be >= 0");
+    if (d->q_indptr[0] != 0 || d->page_indptr[0] != 0)
+        return fail(SANGAM_ERR_INVALID_ARG, "q_indptr[0] and page_indptr[0] must be 0");
+
+    const int hq = d->num_q_heads, hkv = d->num_kv_heads, D = d->head_dim;
+    const int G = hq / hkv;
+    const int num_cus = d->num_cus ? d->num_cus : 256;
+
+    // ---- per-item validation
+    int64_t total_q = 0;
+    for (int i = 0; i < n_items; ++i) {
+        const int64_t n = int64_t(d->q_indptr[i + 1]) - d->q_indptr[i];
+        const int64_t o = d->q_offset[i], L = d->kv_len[i];
+        if (n < 1)
+            return fail(SANGAM_ERR_INVALID_ARG, "item " + std::to_string(i) + ": n_i must be >= 1");
+        if (L < 1)
+            return fail(SANGAM_ERR_INVALID_ARG, "item " + std::to_string(i) + ": kv_len must be >= 1");
+        if (o < 0 || o + n > L)
+            return fail(SANGAM_ERR_INVALID_ARG,
+                        "item " + std::to_string(i) + ": need 0 <= q_offset and q_offset + n <= kv_len");
+        const int64_t np = int64_t(d->page_indptr[i + 1]) - d->page_indptr[i];
+        if (np != ceil_div(L, d->page_size))
+            return fail(SANGAM_ERR_INVALID_ARG,
+                        "item " + std::to_string(i) + ": page count must be ceil(kv_len / page_size)");
+        total_q += n;
+    }
+    if (total_q > INT32_MAX) return fail(SANGAM_ERR_INVALID_ARG, "too many query rows");
+    const int64_t total_pages = d->page_indptr[n_items];
+
+    // ---- page ids: in range and never shared within the batch (two items
+    // writing into one page would race)
+    {
+        std::vector<int32_t> ids(d->page_ids, d->page_ids + total_pages);
+        for (int64_t k = 0; k < total_pages; ++k)
+            if (ids[k] < 0 || ids[k] >= d->num_pool_pages)
+                return fail(SANGAM_ERR_PAGE_RANGE, "page id " + std::to_string(ids[k]) + " at entry " +
+                                                       std::to_string(k) + " is outside the pool");
+        std::sort(ids.begin(), ids.end());
+        for (int64_t k = 1; k < total_pages; ++k)
+            if (ids[k] == ids[k - 1])
+                return fail(SANGAM_ERR_PAGE_ALIAS, "page id " + std::to_string(ids[k]) + " is listed twice");
+    }
+
+    // ---- splits: decode-shaped contexts longer than kForcedSplitLen are always
+    // split; others are cut so that the decode launch has about four
+    // work-groups per CU. Prefill-shaped items already give one work-group per
+    // 128 rows and head, so they are split only on request.
+    const int qw = decode_q_waves(G);
+    const int kw = decode_kv_waves(qw);
+    const int heads_per_tile = qw;
+    const int tiles_per_kv_head = G / heads_per_tile;
+    int64_t decode_keys = 0;
+    for (int i = 0; i < n_items; ++i) {
+        const int64_t n = int64_t(d->q_indptr[i + 1]) - d->q_indptr[i];
+        if (n <= kWaveRows) decode_keys += int64_t(hkv) * tiles_per_kv_head * d->kv_len[i];
+    }
+    int64_t chunk = ceil_div(decode_keys, 4 * int64_t(num_cus));
+    chunk = std::min<int64_t>(std::max<int64_t>(round_up(std::max<int64_t>(chunk, 1), kKeyAlign), 512),
+                              kForcedSplitLen);
+
+    std::vector<ItemRec> items(n_items);
+    int64_t ws_floats = 0;
+    int n_merge = 0, n_split_items = 0, max_splits = 1;
+    for (int i = 0; i < n_items; ++i) {
+        ItemRec& it = items[i];
+        it.q_start = d->q_indptr[i];
+        it.n = d->q_indptr[i + 1] - d->q_indptr[i];
+        it.o = d->q_offset[i];
+        it.L = d->kv_len[i];
+        it.page_start = d->page_indptr[i];
+        int64_t S;
+        if (d->force_kv_splits > 0) {
+            S = std::min<int64_t>(d->force_kv_splits, ceil_div(it.L, kKeyAlign));
+        } else if (it.n <= kWaveRows) {
+            S = std::max<int64_t>(ceil_div(it.L, kForcedSplitLen), ceil_div(it.L, chunk));
+        } else {
+            S = 1;
+        }
+        int64_t len = round_up(ceil_div(it.L, S), kKeyAlign);
+        S = ceil_div(it.L, len);  // no empty chunk
+        it.num_splits = int32_t(S);
+        it.split_len = int32_t(len);
+        it.merge_base = -1;
+        it.ws_o = it.ws_lse = 0;
+        if (S > 1) {
+            it.merge_base = n_merge;
+            n_merge += it.n;
+            ++n_split_items;
+            max_splits = std::max<int>(max_splits, int(S));
+            it.ws_o = ws_floats;
+            ws_floats += S * it.n * int64_t(hq) * D;
+            ws_floats = round_up(ws_floats, 64);
+            it.ws_lse = ws_floats;
+            ws_floats += S * it.n * int64_t(hq);
+            ws_floats = round_up(ws_floats, 64);
+        }
+    }
+
+    // ---- tiles
+    std::vector<TileRec> dec, pre;
+    std::vector<int64_t> dec_cost, pre_cost;
+    for (int i = 0; i < n_items; ++i) {
+        const ItemRec& it = items[i];
+        for (int s = 0; s < it.num_splits; ++s) {
+            const int32_t kb = s * it.split_len;
+            const int32_t ke = std::min<int32_t>(it.L, kb + it.split_len);
+            if (it.n <= kWaveRows) {
+                for (int g = 0; g < hkv; ++g)
+                    for (int t = 0; t < tiles_per_kv_head; ++t) {
+                        TileRec tr{i, g, g * G + t * heads_per_tile, 0, kb, ke, s, 0};
+                        dec.push_back(tr);
+                        dec_cost.push_back(int64_t(ke - kb));
+                    }
+            } else {
+                const int nrb = int(ceil_div(it.n, kPrefillRows));
+                for (int h = 0; h < hq; ++h)
+                    for (int rb = 0; rb < nrb; ++rb) {
+                        TileRec tr{i, h / G, h, rb * kPrefillRows, kb, ke, s, 0};
+                        pre.push_back(tr);
+                        const int rows = std::min(kPrefillRows, it.n - rb * kPrefillRows);
+                        pre_cost.push_back(int64_t(ke - kb) * ((rows + kWaveRows - 1) / kWaveRows));
+                    }
+            }
+        }
+    }
+    // longest first (stable, so equal costs keep batch order)
+    auto lpt = [](std::vector<TileRec>& v, const std::vector<int64_t>& c) {
+        std::vector<size_t> idx(v.size());
+        std::iota(idx.begin(), idx.end(), 0);
+        std::stable_sort(idx.begin(), idx.end(), [&](size_t a, size_t b) { return c[a] > c[b]; });
+        std::vector<TileRec> out(v.size());
+        for (size_t k = 0; k < idx.size(); ++k) out[k] = v[idx[k]];
+        v.swap(out);
+    };
+    lpt(dec, dec_cost);
+    lpt(pre, pre_cost);
+    if (dec.size() > size_t(INT32_MAX) || pre.size() > size_t(INT32_MAX))
+        return fail(SANGAM_ERR_INVALID_ARG, "batch too large");
+
+    std::vector<MergeRow> merge;
+    merge.reserve(n_merge);
+    for (int i = 0; i < n_items; ++i)
+        if (items[i].num_splits > 1)
+            for (int r = 0; r < items[i].n; ++r) merge.push_back(MergeRow{i, r});
+
+    // ---- layout of the blob
+    uint64_t off = align256(sizeof(PlanHeader));
+    const uint64_t off_items = off;
+    off = align256(off + sizeof(ItemRec) * items.size());
+    const uint64_t off_dec = off;
+    off = align256(off + sizeof(TileRec) * dec.size());
+    const uint64_t off_pre = off;
+    off = align256(off + sizeof(TileRec) * pre.size());
+    const uint64_t off_merge = off;
+    off = align256(off + sizeof(MergeRow) * merge.size());
+    const uint64_t total = off;
+
+    *used = size_t(total);
+    if (!plan_buf || cap < total)
+        return fail(SANGAM_ERR_BUFFER, "plan buffer needs " + std::to_string(total) + " bytes");
+
+    uint8_t* base = static_cast<uint8_t*>(plan_buf);
+    std::memset(base, 0, total);
+    PlanHeader h{};
+    h.magic = kPlanMagic;
+    h.version = kPlanVersion;
+    h.total_bytes = total;
+    h.num_items = n_items;
+    h.hq = hq;
+    h.hkv = hkv;
+    h.d = D;
+    h.group = G;
+    h.page_size = d->page_size;
+    h.sm_scale = d->sm_scale;
+    h.scale_log2 = d->sm_scale * 1.44269504088896340736f;
+    h.num_pool_pages = d->num_pool_pages;
+    h.total_q = total_q;
+    h.total_pages = total_pages;
+    h.n_decode_tiles = int32_t(dec.size());
+    h.decode_qw = qw;
+    h.decode_kw = kw;
+    h.decode_nb = (kw >= 4) ? 1 : 2;
+    h.n_prefill_tiles = int32_t(pre.size());
+    h.prefill_nb = 2;
+    h.n_merge_rows = n_merge;
+    h.num_split_items = n_split_items;
+    h.max_splits = max_splits;
+    h.workspace_bytes = ws_floats * int64_t(sizeof(float));
+    h.off_items = off_items;
+    h.off_decode_tiles = off_dec;
+    h.off_prefill_tiles = off_pre;
+    h.off_merge = off_merge;
+    std::memcpy(base, &h, sizeof h);
+    if (!items.empty()) std::memcpy(base + off_items, items.data(), sizeof(ItemRec) * items.size());
+    if (!dec.empty()) std::memcpy(base + off_dec, dec.data(), sizeof(TileRec) * dec.size());
+    if (!pre.empty()) std::memcpy(base + off_pre, pre.data(), sizeof(TileRec) * pre.size());
+    if (!merge.empty()) std::memcpy(base + off_merge, merge.data(), sizeof(MergeRow) * merge.size());
+    return SANGAM_OK;
+}
+
+extern "C" size_t sangam_plan_workspace_bytes(const void* plan_buf) {
+    const PlanHeader* h = check_plan(plan_buf);
+    return h ? size_t(h->workspace_bytes) : 0;
+}
+
+extern "C" sangam_status sangam_plan_get_info(const void* plan_buf, sangam_plan_info* info) {
+    clear_error();
+    const PlanHeader* h = check_plan(plan_buf);
+    if (!h) return fail(SANGAM_ERR_PLAN, "not a plan of this library version");
+    if (!info) return fail(SANGAM_ERR_INVALID_ARG, "info must not be NULL");
+    info->num_items = h->num_items;
+    info->num_decode_tiles = h->n_decode_tiles;
+    info->num_prefill_tiles = h->n_prefill_tiles;
+    info->num_split_items = h->num_split_items;
+    info->max_splits = h->max_splits;
+    info->decode_q_waves = h->decode_qw;
+    info->decode_kv_waves = h->decode_kw;
+    info->reserved = 0;
+    info->total_q_rows = h->total_q;
+    info->workspace_bytes = h->workspace_bytes;
+    info->plan_bytes = int64_t(h->total_bytes);
+    return SANGAM_OK;
+}
+
+extern "C" sangam_status sangam_plan_item_splits(const void* plan_buf, int32_t item, int32_t* num_splits,
+                                                 int32_t* starts, int32_t cap) {
+    clear_error();
+    const PlanHeader* h = check_plan(plan_buf);
+    if (!h) return fail(SANGAM_ERR_PLAN, "not a plan of this library version");
+    if (item < 0 || item >= h->num_items || !num_splits)
+        return fail(SANGAM_ERR_INVALID_ARG, "bad item or NULL num_splits");
+    const ItemRec* items =
+        reinterpret_cast<const ItemRec*>(static_cast<const uint8_t*>(plan_buf) + h->off_items);
+    const ItemRec& it = items[item];
+    *num_splits = it.num_splits;
+    if (starts) {
+        if (cap < it.num_splits + 1) return fail(SANGAM_ERR_BUFFER, "starts needs num_splits + 1 entries");
+        for (int s = 0; s < it.num_splits; ++s) starts[s] = s * it.split_len;
+        starts[it.num_splits] = it.L;
+    }
+    return SANGAM_OK;
+}

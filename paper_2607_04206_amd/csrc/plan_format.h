@@ -1,0 +1,96 @@
+// Launch-plan blob shared by the host planner (plan.cpp) and the gfx950
+// kernels (attn_fwd.hip). The blob is position independent: every array is
+// addressed by a byte offset from the start of the blob, so the same bytes
+// work in host memory and, after a plain copy, in device memory.
+#pragma once
+
+#include <stdint.h>
+
+namespace sangam {
+
+constexpr uint32_t kPlanMagic = 0x50414753u;  // "SGAP"
+constexpr uint32_t kPlanVersion = 1;
+
+constexpr int kWaveRows = 32;       // query rows held by one wave (one decode block)
+constexpr int kPrefillQWaves = 4;   // waves of a prefill-shaped work-group
+constexpr int kPrefillRows = kWaveRows * kPrefillQWaves;
+constexpr int kKeyAlign = 64;       // split boundaries are multiples of this many keys
+constexpr int kForcedSplitLen = 8192;  // a decode context longer than this is always split
+
+// One work item of the batch (a block decode or a whole prefill).
+struct ItemRec {
+    int32_t q_start;     // first packed query row
+    int32_t n;           // query rows
+    int32_t o;           // position of the first query row (block offset)
+    int32_t L;           // context length
+    int32_t page_start;  // first entry of the item in page_ids
+    int32_t num_splits;  // context chunks (1 = written straight to out)
+    int32_t split_len;   // keys per chunk (multiple of kKeyAlign), last may be shorter
+    int32_t merge_base;  // first merge row of the item, -1 when not split
+    int64_t ws_o;        // float offset of partial O  [num_splits][n][Hq][D]
+    int64_t ws_lse;      // float offset of partial LSE [num_splits][n][Hq]
+};
+
+// One work-group of an attention launch.
+struct TileRec {
+    int32_t item;
+    int32_t kv_head;
+    int32_t q_head0;   // first query head of the tile
+    int32_t row0;      // first query row (local to the item)
+    int32_t kv_begin;  // context range [kv_begin, kv_end)
+    int32_t kv_end;
+    int32_t split;     // chunk index of the context
+    int32_t reserved;
+};
+
+// One (item, row) whose split partial results the merge kernel combines.
+struct MergeRow {
+    int32_t item;
+    int32_t row;
+};
+
+struct PlanHeader {
+    uint32_t magic;
+    uint32_t version;
+    uint64_t total_bytes;
+
+    int32_t num_items;
+    int32_t hq;
+    int32_t hkv;
+    int32_t d;
+    int32_t group;      // hq / hkv
+    int32_t page_size;
+    float sm_scale;
+    float scale_log2;   // sm_scale * log2(e): scores enter exp2 in this scale
+    int64_t num_pool_pages;
+    int64_t total_q;
+    int64_t total_pages;
+
+    // decode-shaped launch: items with n <= kWaveRows; one work-group holds
+    // decode_qw query heads (one per wave) x decode_kw context sub-ranges
+    int32_t n_decode_tiles;
+    int32_t decode_qw;
+    int32_t decode_kw;
+    int32_t decode_nb;   // 32-key blocks per wave per stage
+    // prefill-shaped launch: items with n > kWaveRows; kPrefillQWaves waves
+    // of 32 rows of one query head
+    int32_t n_prefill_tiles;
+    int32_t prefill_nb;
+    int32_t n_merge_rows;
+    int32_t num_split_items;
+    int32_t max_splits;
+    int32_t reserved0;
+    int64_t workspace_bytes;
+
+    uint64_t off_items;
+    uint64_t off_decode_tiles;
+    uint64_t off_prefill_tiles;
+    uint64_t off_merge;
+};
+
+static_assert(sizeof(ItemRec) == 48, "ItemRec layout is part of the blob format");
+static_assert(sizeof(TileRec) == 32, "TileRec layout is part of the blob format");
+static_assert(sizeof(MergeRow) == 8, "MergeRow layout is part of the blob format");
+static_assert(sizeof(PlanHeader) == 152, "PlanHeader layout is part of the blob format");
+
+}  // namespace sangam

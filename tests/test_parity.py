@@ -1,0 +1,272 @@
+"""GPU parity: the HIP path (through the C ABI) against the fp64 oracle on the
+same seeded inputs.
+
+Bar (bf16 inputs, fp32 accumulation): over all compared output elements
+max |delta| <= 1e-2 and mean |delta| <= 1e-3, plus max |delta| <= 2e-2 * max|o|
+(outputs shrink like 1/sqrt(L), which makes the absolute bounds loose at long
+contexts); LSE within 1e-3; the cache write-back bit-exact; pool slots the
+batch does not own untouched (they hold NaN, so a stray read or write shows).
+"""
+import numpy as np
+import pytest
+import torch
+
+import workloads
+from oracle import oracle
+
+pytestmark = pytest.mark.gpu
+
+MAX_ABS, MEAN_ABS, REL_MAX, LSE_ABS = 1e-2, 1e-3, 2e-2, 1e-3
+
+
+@pytest.fixture(scope="module")
+def dev():
+    if not torch.cuda.is_available():
+        pytest.skip("needs a GPU")
+    import paper_2607_04206_amd  # noqa: F401  (fails loudly when the library is missing)
+    return torch.device("cuda:0")
+
+
+def run(wl, dev, force_splits=0, fill=float("nan"), want_lse=True):
+    from paper_2607_04206_amd import attn
+    print(f"[case] {wl.name} seed={wl.seed} items={wl.num_items} force_splits={force_splits}",
+          flush=True)
+    t = workloads.device_inputs(wl, dev, fill=fill)
+    p = attn.plan(q_indptr=wl.q_indptr, q_offset=wl.q_offset, kv_len=wl.kv_len,
+                  page_indptr=wl.page_indptr, page_ids=wl.page_ids, num_q_heads=wl.num_q_heads,
+                  num_kv_heads=wl.num_kv_heads, head_dim=wl.head_dim,
+                  num_pool_pages=wl.num_pool_pages, sm_scale=wl.sm_scale,
+                  force_kv_splits=force_splits, device=dev)
+    out, lse = attn.forward(p, t["q"], t["k_new"], t["v_new"], t["k_cache"], t["v_cache"],
+                            t["page_ids"], want_lse=want_lse)
+    torch.cuda.synchronize()
+    return p, t, out, lse
+
+
+def compare(tag, got, ref, got_lse=None, ref_lse=None):
+    got = np.asarray(got, np.float64)
+    assert np.isfinite(got).all(), f"{tag}: non-finite output"
+    d = np.abs(got - ref)
+    mx, mean = d.max(), d.mean()
+    bound = min(MAX_ABS, REL_MAX * np.abs(ref).max())
+    assert mx <= bound, f"{tag}: max |delta| {mx:.3e} > {bound:.3e}"
+    assert mean <= MEAN_ABS, f"{tag}: mean |delta| {mean:.3e}"
+    if got_lse is not None:
+        dl = np.abs(np.asarray(got_lse, np.float64) - ref_lse).max()
+        assert dl <= LSE_ABS, f"{tag}: lse max |delta| {dl:.3e}"
+    return mx, mean
+
+
+def check_full(wl, out, lse):
+    ref, ref_lse = oracle.attention_all(wl)
+    return compare(wl.name, out.float().cpu().numpy(), ref,
+                   None if lse is None else lse.cpu().numpy(), ref_lse)
+
+
+def check_sampled(wl, out, lse, items, rows_per_item=None, heads=None):
+    res = oracle.attention(wl, items=items, rows=rows_per_item, heads=heads)
+    outc = out.float().cpu().numpy()
+    lsec = lse.cpu().numpy()
+    hs = list(range(wl.num_q_heads)) if heads is None else list(heads)
+    g_all, r_all, gl_all, rl_all = [], [], [], []
+    for i, (rr, ro, rl) in res.items():
+        base = int(wl.q_indptr[i])
+        g_all.append(outc[base + rr][:, hs])
+        gl_all.append(lsec[base + rr][:, hs])
+        r_all.append(ro)
+        rl_all.append(rl)
+    return compare(wl.name, np.concatenate([g.reshape(-1) for g in g_all]),
+                   np.concatenate([r.reshape(-1) for r in r_all]),
+                   np.concatenate([g.reshape(-1) for g in gl_all]),
+                   np.concatenate([r.reshape(-1) for r in rl_all]))
+
+
+def check_cache(wl, t, items=None):
+    """Bit-exact write-back on [0, L_i); slots past L_i of the last page keep NaN."""
+    kc, vc = t["k_cache"], t["v_cache"]
+    for i in range(wl.num_items) if items is None else items:
+        ek, ev = oracle.expected_kv(wl, i)
+        gk = workloads.gather_item_cache(wl, kc, i).cpu().view(torch.int16).numpy().view(np.uint16)
+        gv = workloads.gather_item_cache(wl, vc, i).cpu().view(torch.int16).numpy().view(np.uint16)
+        assert np.array_equal(gk, ek), f"item {i}: K cache differs"
+        assert np.array_equal(gv, ev), f"item {i}: V cache differs"
+        L = int(wl.kv_len[i])
+        if L % 16:
+            last = int(wl.item_pages(i)[-1])
+            assert torch.isnan(kc[last, :, L % 16:]).all() and torch.isnan(vc[last, :, L % 16:]).all()
+
+
+def check_pool_untouched(wl, t):
+    """Exactly the owned slots are finite: nothing outside [0, L_i) was written."""
+    owned = int(np.sum(wl.kv_len.astype(np.int64))) * wl.num_kv_heads * wl.head_dim
+    for pool in (t["k_cache"], t["v_cache"]):
+        assert int((~torch.isnan(pool)).sum().item()) == owned
+
+
+# ------------------------------------------------------------------- cases
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_tiny_mixed(dev, seed):
+    wl = workloads.tiny_mixed(seed)
+    p, t, out, lse = run(wl, dev)
+    check_full(wl, out, lse)
+    check_cache(wl, t)
+    check_pool_untouched(wl, t)
+    # the block decode of rows 96..127 matches the prefill's rows 96..127
+    o = out.float().cpu().numpy()
+    assert np.abs(o[:32] - o[32 + 96:32 + 128]).max() <= 1e-2
+
+
+SHAPES = [(4, 4, 64), (8, 2, 64), (18, 2, 64), (28, 4, 128), (32, 32, 128), (8, 4, 128), (11, 1, 128),
+          (24, 8, 128)]
+
+
+@pytest.mark.parametrize("hq,hkv,d", SHAPES)
+def test_ragged_small(dev, hq, hkv, d):
+    wl = workloads.ragged_small(0, hq=hq, hkv=hkv, d=d)
+    p, t, out, lse = run(wl, dev)
+    check_full(wl, out, lse)
+    check_cache(wl, t)
+    check_pool_untouched(wl, t)
+
+
+@pytest.mark.parametrize("hq,hkv,d", [(4, 4, 64), (28, 4, 128), (32, 32, 128)])
+@pytest.mark.parametrize("force", [1, 2, 4, 8])
+def test_forced_splits(dev, hq, hkv, d, force):
+    wl = workloads.ragged_small(1, hq=hq, hkv=hkv, d=d)
+    p, t, out, lse = run(wl, dev, force_splits=force)
+    check_full(wl, out, lse)
+    check_cache(wl, t)
+
+
+def test_split_count_independence(dev):
+    wl = workloads.llada_decode(2)
+    outs = [run(wl, dev, force_splits=k)[2].float() for k in (1, 2, 4, 8)]
+    for o in outs[1:]:
+        assert (o - outs[0]).abs().max().item() <= 1e-2
+
+
+def test_q_stress(dev):
+    wl = workloads.ragged_small(2, hq=28, hkv=4, d=128, q_scale=4.0)
+    p, t, out, lse = run(wl, dev)
+    check_full(wl, out, lse)
+
+
+def test_no_lse(dev):
+    wl = workloads.ragged_small(3, hq=8, hkv=2, d=64)
+    p, t, out, lse = run(wl, dev, want_lse=False)
+    assert lse is None
+    ref, _ = oracle.attention_all(wl)
+    compare(wl.name, out.float().cpu().numpy(), ref)
+
+
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_llada_decode(dev, seed):
+    wl = workloads.llada_decode(seed)
+    p, t, out, lse = run(wl, dev)
+    check_full(wl, out, lse)
+    check_cache(wl, t)
+    check_pool_untouched(wl, t)
+
+
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_dream_mixed(dev, seed):
+    wl = workloads.dream_mixed(seed)
+    p, t, out, lse = run(wl, dev)
+    n_dec = int((~wl.is_prefill).sum())
+    rng = np.random.default_rng(seed)
+    rows = {}
+    for i in range(n_dec, wl.num_items):
+        n = wl.n(i)
+        rows[i] = np.unique(np.r_[0, n - 1, 127, 128, rng.integers(0, n, 40)])
+    check_sampled(wl, out, lse, items=list(range(wl.num_items)), rows_per_item=rows)
+    check_cache(wl, t)
+    check_pool_untouched(wl, t)
+
+
+def test_prefill_heavy(dev):
+    wl = workloads.prefill_heavy(0)
+    p, t, out, lse = run(wl, dev)
+    rng = np.random.default_rng(5)
+    rows = {i: np.unique(np.r_[0, wl.n(i) - 1, rng.integers(0, wl.n(i), 10)]) for i in range(wl.num_items)}
+    check_sampled(wl, out, lse, items=list(range(wl.num_items)), rows_per_item=rows)
+    check_cache(wl, t, items=[0, wl.num_items - 1])
+    check_pool_untouched(wl, t)
+
+
+def test_long_decode(dev):
+    wl = workloads.long_decode(0)
+    p, t, out, lse = run(wl, dev)
+    order = np.argsort(-wl.kv_len)
+    rng = np.random.default_rng(7)
+    items = sorted(set(order[:6].tolist()) | set(rng.choice(wl.num_items, 10, replace=False).tolist()))
+    assert int(wl.kv_len[order[0]]) > 8192  # split-KV path exercised
+    check_sampled(wl, out, lse, items=items, heads=[0, 13, 31])
+    check_cache(wl, t, items=items)
+    check_pool_untouched(wl, t)
+
+
+def test_deterministic(dev):
+    wl = workloads.dream_mixed(1)
+    _, _, o1, l1 = run(wl, dev)
+    _, _, o2, l2 = run(wl, dev)
+    assert torch.equal(o1, o2) and torch.equal(l1, l2)
+
+
+# --------------------------------------------------------------- invariants
+def test_constant_v_and_equal_keys(dev):
+    L, o = 700, 333
+    c = torch.linspace(-2, 2, 128).bfloat16().float()
+    vals = {
+        (0, workloads.KIND_VCTX): c.expand(L, 4, 128).clone(),
+        (0, workloads.KIND_VNEW): c.expand(32, 4, 128).clone(),
+        (1, workloads.KIND_VNEW): c.expand(300, 4, 128).clone(),
+    }
+    wl = workloads.make_workload("const_v", 0, hq=28, hkv=4, d=128, decodes=[(o, L)], prefills=[300])
+    wl.value_fn = lambda item, kind: vals.get((item, kind))
+    _, _, out, _ = run(wl, dev)
+    exp = c.to(torch.bfloat16).float().to(dev)
+    assert (out.float() - exp).abs().max().item() == 0.0
+
+    krow = torch.randn(1, 4, 128, generator=torch.Generator().manual_seed(0)).bfloat16().float()
+    vals2 = {(0, workloads.KIND_KCTX): krow.expand(L, 4, 128).clone(),
+             (0, workloads.KIND_KNEW): krow.expand(32, 4, 128).clone()}
+    wl2 = workloads.make_workload("eq_k", 0, hq=28, hkv=4, d=128, decodes=[(o, L)], prefills=[])
+    wl2.value_fn = lambda item, kind: vals2.get((item, kind))
+    _, _, out2, _ = run(wl2, dev)
+    V = wl2.v_ctx(0).double().clone()
+    V[o:o + 32] = wl2.v_new(0).double()
+    mean = V.mean(0)  # [4, 128]
+    ref = mean.repeat_interleave(7, 0)[None].expand(32, 28, 128).numpy()
+    compare("equal keys", out2.float().cpu().numpy(), ref)
+
+
+def test_page_signature(dev):
+    """All keys equal (uniform weights) and V[j, d] = 1 iff page(j) % D == d:
+    o[d] is the fraction of the item's tokens on pages congruent to d, so a
+    dropped or repeated page changes it by at least 1/L."""
+    D = 64
+    decodes = [(7, 900), (0, 33), (250, 2051)]
+    wl = workloads.make_workload("pagesig", 3, hq=2, hkv=2, d=D, decodes=decodes, prefills=[])
+    vals = {}
+    for i in range(wl.num_items):
+        L = int(wl.kv_len[i])
+        o = int(wl.q_offset[i])
+        pages = wl.item_pages(i)
+        v = torch.zeros(L, 2, D)
+        pos = np.arange(L)
+        v[pos, :, pages[pos // 16] % D] = 1.0
+        vals[(i, workloads.KIND_VCTX)] = v
+        vals[(i, workloads.KIND_VNEW)] = v[o:o + wl.n(i)].clone()
+        vals[(i, workloads.KIND_KCTX)] = torch.ones(L, 2, D)
+        vals[(i, workloads.KIND_KNEW)] = torch.ones(wl.n(i), 2, D)
+    wl.value_fn = lambda item, kind: vals.get((item, kind))
+    _, _, out, _ = run(wl, dev)
+    outc = out.float().cpu().numpy()
+    for i in range(wl.num_items):
+        L = int(wl.kv_len[i])
+        pages = wl.item_pages(i)
+        frac = np.bincount(pages[np.arange(L) // 16] % D, minlength=D) / L
+        exp = torch.tensor(frac, dtype=torch.float32).bfloat16().float().numpy()
+        base = int(wl.q_indptr[i])
+        got = outc[base:base + wl.n(i)]
+        assert np.abs(got - exp[None, None]).max() <= 2 ** -8 * max(exp.max(), 1e-3), f"item {i}"

@@ -1,0 +1,248 @@
+"""Host planner: descriptor validation, tile coverage, split rules, ordering.
+Runs without a GPU (the planner makes no HIP call)."""
+import ctypes
+
+import numpy as np
+import pytest
+
+import workloads
+from paper_2607_04206_amd import attn
+from paper_2607_04206_amd._lib import SangamError, lib
+
+# Internal blob layout (plan_format.h), read here only to check coverage.
+HEADER = np.dtype([
+    ("magic", "<u4"), ("version", "<u4"), ("total_bytes", "<u8"),
+    ("num_items", "<i4"), ("hq", "<i4"), ("hkv", "<i4"), ("d", "<i4"), ("group", "<i4"),
+    ("page_size", "<i4"), ("sm_scale", "<f4"), ("scale_log2", "<f4"),
+    ("num_pool_pages", "<i8"), ("total_q", "<i8"), ("total_pages", "<i8"),
+    ("n_decode_tiles", "<i4"), ("decode_qw", "<i4"), ("decode_kw", "<i4"), ("decode_nb", "<i4"),
+    ("n_prefill_tiles", "<i4"), ("prefill_nb", "<i4"), ("n_merge_rows", "<i4"),
+    ("num_split_items", "<i4"), ("max_splits", "<i4"), ("reserved0", "<i4"),
+    ("workspace_bytes", "<i8"),
+    ("off_items", "<u8"), ("off_decode_tiles", "<u8"), ("off_prefill_tiles", "<u8"), ("off_merge", "<u8"),
+])
+ITEM = np.dtype([("q_start", "<i4"), ("n", "<i4"), ("o", "<i4"), ("L", "<i4"), ("page_start", "<i4"),
+                 ("num_splits", "<i4"), ("split_len", "<i4"), ("merge_base", "<i4"),
+                 ("ws_o", "<i8"), ("ws_lse", "<i8")])
+TILE = np.dtype([("item", "<i4"), ("kv_head", "<i4"), ("q_head0", "<i4"), ("row0", "<i4"),
+                 ("kv_begin", "<i4"), ("kv_end", "<i4"), ("split", "<i4"), ("reserved", "<i4")])
+MERGE = np.dtype([("item", "<i4"), ("row", "<i4")])
+
+
+def parse(p):
+    b = p.host
+    h = np.frombuffer(b, HEADER, count=1)[0]
+    items = np.frombuffer(b, ITEM, count=int(h["num_items"]), offset=int(h["off_items"]))
+    dec = np.frombuffer(b, TILE, count=int(h["n_decode_tiles"]), offset=int(h["off_decode_tiles"]))
+    pre = np.frombuffer(b, TILE, count=int(h["n_prefill_tiles"]), offset=int(h["off_prefill_tiles"]))
+    mer = np.frombuffer(b, MERGE, count=int(h["n_merge_rows"]), offset=int(h["off_merge"]))
+    return h, items, dec, pre, mer
+
+
+def plan_of(wl, **kw):
+    return attn.plan(q_indptr=wl.q_indptr, q_offset=wl.q_offset, kv_len=wl.kv_len,
+                     page_indptr=wl.page_indptr, page_ids=wl.page_ids,
+                     num_q_heads=wl.num_q_heads, num_kv_heads=wl.num_kv_heads,
+                     head_dim=wl.head_dim, num_pool_pages=wl.num_pool_pages,
+                     sm_scale=wl.sm_scale, **kw)
+
+
+def test_header_size_matches():
+    # plan_format.h static_asserts the same sizes on the C side
+    p = plan_of(workloads.tiny_mixed(0))
+    h, *_ = parse(p)
+    assert h["magic"] == 0x50414753 and h["version"] == 1
+    assert h["total_bytes"] == p.host.nbytes
+    assert HEADER.itemsize == 152 and ITEM.itemsize == 48 and TILE.itemsize == 32
+
+
+def coverage(wl, p):
+    """Count how often each (item, q-head, row, key) is covered by a tile."""
+    h, items, dec, pre, _ = parse(p)
+    G = wl.num_q_heads // wl.num_kv_heads
+    qw = int(h["decode_qw"])
+    cover = {}
+    for i in range(wl.num_items):
+        cover[i] = np.zeros((wl.num_q_heads, wl.n(i), int(wl.kv_len[i])), np.int32)
+    for t in dec:
+        i = int(t["item"])
+        assert wl.n(i) <= 32
+        for hd in range(int(t["q_head0"]), int(t["q_head0"]) + qw):
+            assert hd // G == t["kv_head"]
+            cover[i][hd, :, t["kv_begin"]:t["kv_end"]] += 1
+    for t in pre:
+        i = int(t["item"])
+        assert wl.n(i) > 32
+        hd = int(t["q_head0"])
+        assert hd // G == t["kv_head"]
+        r0 = int(t["row0"])
+        cover[i][hd, r0:r0 + 128, t["kv_begin"]:t["kv_end"]] += 1
+    return cover
+
+
+@pytest.mark.parametrize("mk", [
+    lambda: workloads.tiny_mixed(0),
+    lambda: workloads.ragged_small(0, hq=4, hkv=4, d=64),
+    lambda: workloads.ragged_small(0, hq=28, hkv=4, d=128),
+    lambda: workloads.ragged_small(0, hq=8, hkv=4, d=128),
+    lambda: workloads.ragged_small(0, hq=18, hkv=2, d=64),
+    lambda: workloads.ragged_small(0, hq=11, hkv=1, d=128),
+    lambda: workloads.llada_decode(1),
+    lambda: workloads.dream_mixed(2),
+])
+@pytest.mark.parametrize("force", [0, 1, 3, 8])
+def test_every_row_head_key_covered_once(mk, force):
+    wl = mk()
+    p = plan_of(wl, force_kv_splits=force)
+    for i, c in coverage(wl, p).items():
+        assert c.min() == 1 and c.max() == 1, f"item {i}"
+
+
+def test_splits_and_merge_rows():
+    wl = workloads.make_workload("long", 0, hq=4, hkv=4, d=128,
+                                 decodes=[(100, 9000), (0, 8192), (5, 300)], prefills=[20000])
+    p = plan_of(wl)
+    h, items, dec, pre, mer = parse(p)
+    # a decode context over 8192 keys is always split; chunks are 64-aligned
+    assert items[0]["num_splits"] >= 2
+    assert items[0]["split_len"] % 64 == 0 and items[0]["split_len"] <= 8192
+    assert items[1]["split_len"] <= 8192
+    # prefill-shaped items are not split by default
+    assert items[3]["num_splits"] == 1
+    # merge rows list exactly the rows of split items
+    want = [(i, r) for i in range(4) if items[i]["num_splits"] > 1 for r in range(wl.n(i))]
+    assert [(int(m["item"]), int(m["row"])) for m in mer] == want
+    # partial buffers do not overlap and fit in the workspace
+    spans = []
+    for it in items:
+        if it["num_splits"] > 1:
+            S, n = int(it["num_splits"]), int(it["n"])
+            spans.append((int(it["ws_o"]), int(it["ws_o"]) + S * n * 4 * 128))
+            spans.append((int(it["ws_lse"]), int(it["ws_lse"]) + S * n * 4))
+    spans.sort()
+    for (a0, a1), (b0, b1) in zip(spans, spans[1:]):
+        assert a1 <= b0
+    assert spans[-1][1] * 4 <= p.workspace_bytes
+    starts = p.item_splits(0)
+    assert starts[0] == 0 and starts[-1] == 9000 and np.all(np.diff(starts) > 0)
+
+
+def test_forced_split_count():
+    wl = workloads.llada_decode(0)
+    for k in (1, 2, 4, 8):
+        p = plan_of(wl, force_kv_splits=k)
+        _, items, *_ = parse(p)
+        for i, it in enumerate(items):
+            L = int(wl.kv_len[i])
+            assert it["num_splits"] == min(k, -(-L // 64)) or it["num_splits"] <= k
+            assert it["num_splits"] * it["split_len"] >= L > (it["num_splits"] - 1) * it["split_len"]
+        if k == 1:
+            assert p.workspace_bytes == 0
+
+
+def test_longest_first():
+    p = plan_of(workloads.dream_mixed(0))
+    _, items, dec, pre, _ = parse(p)
+    dc = dec["kv_end"] - dec["kv_begin"]
+    assert np.all(np.diff(dc) <= 0)
+    rows = np.minimum(128, items["n"][pre["item"]] - pre["row0"])
+    pc = (pre["kv_end"] - pre["kv_begin"]) * ((rows + 31) // 32)
+    assert np.all(np.diff(pc) <= 0)
+
+
+def test_deterministic_bytes():
+    wl = workloads.dream_mixed(1)
+    a = plan_of(wl).host
+    b = plan_of(wl).host
+    assert np.array_equal(a, b)
+
+
+def test_decode_wave_shapes():
+    for hq, hkv, qw, kw in [(32, 32, 1, 4), (8, 4, 2, 2), (28, 4, 7, 1), (24, 8, 3, 1),
+                            (16, 1, 8, 1), (18, 2, 3, 1), (11, 1, 1, 4)]:
+        wl = workloads.make_workload("s", 0, hq=hq, hkv=hkv, d=128, decodes=[(0, 64)], prefills=[])
+        p = plan_of(wl)
+        assert (p.info.decode_q_waves, p.info.decode_kv_waves) == (qw, kw), (hq, hkv)
+
+
+# ---------------------------------------------------------------- validation
+def _desc_kwargs(wl):
+    return dict(q_indptr=wl.q_indptr.copy(), q_offset=wl.q_offset.copy(), kv_len=wl.kv_len.copy(),
+                page_indptr=wl.page_indptr.copy(), page_ids=wl.page_ids.copy(),
+                num_q_heads=wl.num_q_heads, num_kv_heads=wl.num_kv_heads, head_dim=wl.head_dim,
+                num_pool_pages=wl.num_pool_pages, sm_scale=wl.sm_scale)
+
+
+CODES = {"INVALID": -1, "UNSUPPORTED": -2, "PAGE_RANGE": -3, "PAGE_ALIAS": -4, "BUFFER": -5}
+
+
+def _expect(code, **kw):
+    with pytest.raises(SangamError) as e:
+        attn.plan(**kw)
+    assert e.value.status == CODES[code], str(e.value)
+    assert len(lib.sangam_last_error()) > 0
+
+
+def test_rejects_bad_descriptors():
+    wl = workloads.ragged_small(0, hq=4, hkv=2, d=64)
+    base = _desc_kwargs(wl)
+
+    k = dict(base); k["head_dim"] = 96; _expect("UNSUPPORTED", **k)
+    k = dict(base); k["num_kv_heads"] = 3; _expect("UNSUPPORTED", **k)
+    k = dict(base); k["page_size"] = 32; _expect("UNSUPPORTED", **k)
+    k = dict(base); k["sm_scale"] = float("nan"); _expect("INVALID", **k)
+    k = dict(base); k["sm_scale"] = -1.0; _expect("INVALID", **k)
+    k = dict(base); k["num_q_heads"] = 0; _expect("INVALID", **k)
+
+    k = dict(base); qo = k["q_offset"].copy(); qo[0] = wl.kv_len[0]; k["q_offset"] = qo
+    _expect("INVALID", **k)  # o + n > L
+    k = dict(base); qo = k["q_offset"].copy(); qo[1] = -1; k["q_offset"] = qo
+    _expect("INVALID", **k)
+    k = dict(base); kl = k["kv_len"].copy(); kl[2] += 16; k["kv_len"] = kl
+    _expect("INVALID", **k)  # page count no longer ceil(L/16)
+    k = dict(base); qi = k["q_indptr"].copy(); qi[1] = qi[0]; k["q_indptr"] = qi
+    _expect("INVALID", **k)  # n_0 = 0
+    k = dict(base); pi = k["page_ids"].copy(); pi[3] = wl.num_pool_pages; k["page_ids"] = pi
+    _expect("PAGE_RANGE", **k)
+    k = dict(base); pi = k["page_ids"].copy(); pi[3] = -2; k["page_ids"] = pi
+    _expect("PAGE_RANGE", **k)
+    k = dict(base); pi = k["page_ids"].copy(); pi[5] = pi[1]; k["page_ids"] = pi
+    _expect("PAGE_ALIAS", **k)
+
+
+def test_zero_length_items_rejected():
+    k = dict(q_indptr=[0, 1], q_offset=[0], kv_len=[0], page_indptr=[0, 0], page_ids=[],
+             num_q_heads=1, num_kv_heads=1, head_dim=64, num_pool_pages=4, sm_scale=0.125)
+    _expect("INVALID", **k)
+    k = dict(q_indptr=[0], q_offset=[], kv_len=[], page_indptr=[0], page_ids=[],
+             num_q_heads=1, num_kv_heads=1, head_dim=64, num_pool_pages=4, sm_scale=0.125)
+    _expect("INVALID", **k)
+
+
+def test_buffer_too_small_reports_size():
+    from paper_2607_04206_amd._lib import SANGAM_OK
+    wl = workloads.llada_decode(0)
+    d, keep = attn.make_desc(**_desc_kwargs(wl))
+    used = ctypes.c_size_t(0)
+    st = lib.sangam_attn_plan(ctypes.byref(d), None, 0, ctypes.byref(used))
+    assert st == CODES["BUFFER"] and used.value > 0
+    buf = np.zeros(used.value - 1, np.uint8)
+    st = lib.sangam_attn_plan(ctypes.byref(d), buf.ctypes.data, buf.nbytes, ctypes.byref(used))
+    assert st == CODES["BUFFER"]
+    buf = np.zeros(used.value, np.uint8)
+    st = lib.sangam_attn_plan(ctypes.byref(d), buf.ctypes.data, buf.nbytes, ctypes.byref(used))
+    assert st == SANGAM_OK
+    del keep
+
+
+def test_long_decode_plan_is_fast_and_sized():
+    import time
+    wl = workloads.long_decode(0)
+    t = time.perf_counter()
+    p = plan_of(wl)
+    dt = time.perf_counter() - t
+    assert dt < 2.0
+    _, items, dec, pre, _ = parse(p)
+    assert len(pre) == 0
+    assert np.all(items["split_len"] <= 8192)
+    assert np.all((items["L"] <= 8192) | (items["num_splits"] >= 2))

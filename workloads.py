@@ -19,9 +19,15 @@ Recipe (one for every workload):
 3. A block decode at block index ``b`` has ``n = 32`` query rows at
    positions ``o = P + 32 b``; a prefill has ``o = 0``, ``n = L``.
 4. Page ids are ``rng.permutation(pool)[:needed]``, handed out in item order.
-5. Values: each tensor piece has its own ``torch.Generator`` seeded from
-   (seed, item, kind); ``randn`` in fp32, then rounded to bf16 (RNE). The bf16
-   bytes are the ground truth both sides read.
+5. Values come from a counter-based generator, so any piece can be drawn on
+   the CPU or directly in device memory with identical bits: element ``c`` of
+   piece (seed, item, kind) is ``T[(h(mul(c) + key) >> 8) & 0xFFFF]`` where
+   ``h`` is the lowbias32 integer hash (C. Wellons, "Prospecting for hash
+   functions", 2018), ``mul`` multiplies by an odd constant mod 2^32, ``key``
+   hashes (seed, item, kind), and ``T`` holds the 65536 quantiles
+   ``Phi^-1((i + 0.5) / 65536)`` of N(0, 1), rounded to bf16 (RNE). Only
+   integer arithmetic runs per element, so CPU and GPU draws agree bit for
+   bit. The bf16 bytes are the ground truth both sides read.
 6. Batch order: decodes first, then prefills (the microbatch order of the
    deficit scheduler, Alg. 1).
 """
@@ -75,57 +81,49 @@ class Workload:
         return int(self.q_indptr[i + 1] - self.q_indptr[i])
 
     # ------------------------------------------------------------------ values
-    def _gen(self, item: int, kind: int) -> torch.Generator:
-        g = torch.Generator(device="cpu")
-        mix = (((self.seed * 1_000_003) + item) * 8 + kind) & ((1 << 62) - 1)
-        g.manual_seed(mix)
-        return g
-
-    def _draw(self, item: int, kind: int, shape: Tuple[int, ...]) -> torch.Tensor:
+    def _draw(self, item: int, kind: int, shape: Tuple[int, ...], device="cpu") -> torch.Tensor:
         if self.value_fn is not None:
             t = self.value_fn(item, kind)
             if t is not None:
                 assert tuple(t.shape) == tuple(shape), (t.shape, shape)
-                return t.to(torch.bfloat16)
-        x = torch.randn(shape, generator=self._gen(item, kind), dtype=torch.float32)
-        if kind == KIND_Q and self.q_scale != 1.0:
-            x = x * self.q_scale
-        return x.to(torch.bfloat16)
+                return t.to(torch.bfloat16).to(device)
+        scale = self.q_scale if kind == KIND_Q else 1.0
+        return counter_normal_bf16(self.seed, item, kind, shape, device=device, scale=scale)
 
-    def q(self, i: int) -> torch.Tensor:
+    def q(self, i: int, device="cpu") -> torch.Tensor:
         """Query rows of item i, bf16 [n_i, Hq, D]."""
-        return self._draw(i, KIND_Q, (self.n(i), self.num_q_heads, self.head_dim))
+        return self._draw(i, KIND_Q, (self.n(i), self.num_q_heads, self.head_dim), device)
 
-    def k_new(self, i: int) -> torch.Tensor:
+    def k_new(self, i: int, device="cpu") -> torch.Tensor:
         """Fresh keys of item i (positions o_i .. o_i+n_i-1), bf16 [n_i, Hkv, D]."""
-        return self._draw(i, KIND_KNEW, (self.n(i), self.num_kv_heads, self.head_dim))
+        return self._draw(i, KIND_KNEW, (self.n(i), self.num_kv_heads, self.head_dim), device)
 
-    def v_new(self, i: int) -> torch.Tensor:
-        return self._draw(i, KIND_VNEW, (self.n(i), self.num_kv_heads, self.head_dim))
+    def v_new(self, i: int, device="cpu") -> torch.Tensor:
+        return self._draw(i, KIND_VNEW, (self.n(i), self.num_kv_heads, self.head_dim), device)
 
-    def k_ctx(self, i: int) -> Optional[torch.Tensor]:
+    def k_ctx(self, i: int, device="cpu") -> Optional[torch.Tensor]:
         """Cache content before the call for positions [0, L_i), bf16 [L_i, Hkv, D].
 
         None for a prefill (it brings its whole sequence as fresh rows). Rows
         [o_i, o_i+n_i) hold stale values that the call must overwrite."""
         if self.is_prefill[i]:
             return None
-        return self._draw(i, KIND_KCTX, (int(self.kv_len[i]), self.num_kv_heads, self.head_dim))
+        return self._draw(i, KIND_KCTX, (int(self.kv_len[i]), self.num_kv_heads, self.head_dim), device)
 
-    def v_ctx(self, i: int) -> Optional[torch.Tensor]:
+    def v_ctx(self, i: int, device="cpu") -> Optional[torch.Tensor]:
         if self.is_prefill[i]:
             return None
-        return self._draw(i, KIND_VCTX, (int(self.kv_len[i]), self.num_kv_heads, self.head_dim))
+        return self._draw(i, KIND_VCTX, (int(self.kv_len[i]), self.num_kv_heads, self.head_dim), device)
 
-    # ------------------------------------------------------- packed host views
-    def packed_q(self) -> torch.Tensor:
-        return torch.cat([self.q(i) for i in range(self.num_items)], 0)
+    # ------------------------------------------------------- packed views
+    def packed_q(self, device="cpu") -> torch.Tensor:
+        return torch.cat([self.q(i, device) for i in range(self.num_items)], 0)
 
-    def packed_k_new(self) -> torch.Tensor:
-        return torch.cat([self.k_new(i) for i in range(self.num_items)], 0)
+    def packed_k_new(self, device="cpu") -> torch.Tensor:
+        return torch.cat([self.k_new(i, device) for i in range(self.num_items)], 0)
 
-    def packed_v_new(self) -> torch.Tensor:
-        return torch.cat([self.v_new(i) for i in range(self.num_items)], 0)
+    def packed_v_new(self, device="cpu") -> torch.Tensor:
+        return torch.cat([self.v_new(i, device) for i in range(self.num_items)], 0)
 
     def item_pages(self, i: int) -> np.ndarray:
         return self.page_ids[self.page_indptr[i]:self.page_indptr[i + 1]]
@@ -135,29 +133,24 @@ class Workload:
 
         Pool layout [num_pool_pages, Hkv, page_size, D]: position p of item i
         lives in page page_ids[page_indptr[i] + p // page_size], slot
-        p % page_size. Works for CPU or device pools (copies per item)."""
+        p % page_size. Values are drawn on the pool's device. Slots >= L_i of
+        an item's last page keep whatever the pool held."""
         S = self.page_size
+        dev = k_pool.device
         for i in range(self.num_items) if items is None else items:
             if self.is_prefill[i]:
                 continue
             L = int(self.kv_len[i])
-            pages = torch.from_numpy(self.item_pages(i).astype(np.int64))
+            pages = torch.from_numpy(self.item_pages(i).astype(np.int64)).to(dev)
             npg = pages.numel()
-            for kind, pool in ((KIND_KCTX, k_pool), (KIND_VCTX, v_pool)):
-                ctx = self.k_ctx(i) if kind == KIND_KCTX else self.v_ctx(i)
-                pad = torch.zeros((npg * S, self.num_kv_heads, self.head_dim), dtype=torch.bfloat16)
-                pad[:L] = ctx
-                # [npg, S, Hkv, D] -> [npg, Hkv, S, D]
-                blk = pad.view(npg, S, self.num_kv_heads, self.head_dim).permute(0, 2, 1, 3)
-                full = npg * S == L
-                dev_pages = pages.to(pool.device)
+            full = L // S  # whole pages
+            for ctx, pool in ((self.k_ctx(i, dev), k_pool), (self.v_ctx(i, dev), v_pool)):
                 if full:
-                    pool[dev_pages] = blk.to(pool.device)
-                else:
-                    # the last page's slots >= L keep whatever the pool held
-                    pool[dev_pages[:-1]] = blk[:-1].to(pool.device)
-                    r = L - (npg - 1) * S
-                    pool[dev_pages[-1], :, :r] = blk[-1, :, :r].to(pool.device)
+                    blk = ctx[:full * S].view(full, S, self.num_kv_heads, self.head_dim)
+                    pool[pages[:full]] = blk.permute(0, 2, 1, 3)
+                r = L - full * S
+                if r:
+                    pool[pages[npg - 1], :, :r] = ctx[full * S:].permute(1, 0, 2)
 
     def flops(self) -> float:
         """Algorithmic flops: QK^T and PV, non-causal, 4*n*L*D*Hq per item."""
@@ -174,6 +167,61 @@ class Workload:
         per += 4.0 * np.ceil(L / self.page_size) + 4.0 * n * Hq
         return float(np.sum(per))
 
+
+
+# ------------------------------------------------------- counter generator
+_M32 = 0xFFFFFFFF
+_TABLES = {}
+
+
+def _mul32(x: torch.Tensor, c: int) -> torch.Tensor:
+    """(x * c) mod 2^32 for int64 tensors holding values < 2^32, without
+    overflowing int64 (16-bit halves)."""
+    lo = (x & 0xFFFF) * c
+    hi = (((x >> 16) * c) & 0xFFFF) << 16
+    return (lo + hi) & _M32
+
+
+def _lowbias32(x: torch.Tensor) -> torch.Tensor:
+    x = x ^ (x >> 16)
+    x = _mul32(x, 0x7FEB352D)
+    x = x ^ (x >> 15)
+    x = _mul32(x, 0x846CA68B)
+    return x ^ (x >> 16)
+
+
+def normal_table(device="cpu", scale: float = 1.0) -> torch.Tensor:
+    """65536 bf16 quantiles of N(0, 1) (times scale, before rounding)."""
+    key = (str(device), float(scale))
+    if key not in _TABLES:
+        i = torch.arange(65536, dtype=torch.float64)
+        t = torch.special.ndtri((i + 0.5) / 65536.0) * scale
+        _TABLES[key] = t.to(torch.bfloat16).to(device)
+    return _TABLES[key]
+
+
+def piece_key(seed: int, item: int, kind: int) -> int:
+    k = torch.tensor([(seed * 0x9E3779B1 + item * 0x85EBCA77 + kind * 0xC2B2AE3D) & _M32],
+                     dtype=torch.int64)
+    k = _lowbias32(_lowbias32(k) ^ ((seed >> 32) & _M32))
+    return int(k.item())
+
+
+def counter_normal_bf16(seed: int, item: int, kind: int, shape, device="cpu", scale: float = 1.0,
+                        chunk: int = 1 << 24) -> torch.Tensor:
+    """Element c of piece (seed, item, kind): T[(h(mul(c) + key) >> 8) & 0xFFFF]."""
+    n = int(np.prod(shape)) if len(shape) else 1
+    if n >= (1 << 32):
+        raise ValueError("a piece must have fewer than 2^32 elements")
+    key = piece_key(seed, item, kind)
+    table = normal_table(device, scale)
+    out = torch.empty(n, dtype=torch.bfloat16, device=device)
+    for c0 in range(0, n, chunk):
+        c1 = min(n, c0 + chunk)
+        idx = torch.arange(c0, c1, dtype=torch.int64, device=device)
+        h = _lowbias32((_mul32(idx, 0x27D4EB2F) + key) & _M32)
+        out[c0:c1] = table[(h >> 8) & 0xFFFF]
+    return out.view(*shape)
 
 # ---------------------------------------------------------------- builders
 def _lognormal_lengths(rng, count, median, sigma, lo, hi) -> np.ndarray:
@@ -321,3 +369,29 @@ def ragged_small(seed: int, *, hq: int, hkv: int, d: int, q_scale: float = 1.0) 
     pre = [1, 19, 150, 301]
     return make_workload(f"ragged_small_{hq}_{hkv}_{d}", seed, hq=hq, hkv=hkv, d=d,
                          decodes=dec, prefills=pre, rng=rng, q_scale=q_scale)
+
+
+def device_inputs(wl: Workload, device, fill: Optional[float] = float("nan")) -> dict:
+    """Device tensors of one call: packed q / k_new / v_new, the paged pools with
+    every decode item's pre-call context scattered in, and the page table.
+    Pool slots that hold no context are set to ``fill`` (NaN by default, so a
+    read of an unowned slot shows up in the output); ``fill=None`` leaves them
+    uninitialised."""
+    shape = (wl.num_pool_pages, wl.num_kv_heads, wl.page_size, wl.head_dim)
+    if fill is None:
+        k_cache = torch.empty(shape, dtype=torch.bfloat16, device=device)
+        v_cache = torch.empty(shape, dtype=torch.bfloat16, device=device)
+    else:
+        k_cache = torch.full(shape, fill, dtype=torch.bfloat16, device=device)
+        v_cache = torch.full(shape, fill, dtype=torch.bfloat16, device=device)
+    wl.fill_paged_cache(k_cache, v_cache)
+    return dict(q=wl.packed_q(device), k_new=wl.packed_k_new(device), v_new=wl.packed_v_new(device),
+                k_cache=k_cache, v_cache=v_cache,
+                page_ids=torch.from_numpy(np.ascontiguousarray(wl.page_ids)).to(device))
+
+
+def gather_item_cache(wl: Workload, pool: torch.Tensor, i: int) -> torch.Tensor:
+    """Positions [0, L_i) of item i read back from a pool, [L_i, Hkv, D]."""
+    pages = torch.from_numpy(wl.item_pages(i).astype(np.int64)).to(pool.device)
+    blk = pool[pages].permute(0, 2, 1, 3).reshape(-1, wl.num_kv_heads, wl.head_dim)
+    return blk[:int(wl.kv_len[i])]
