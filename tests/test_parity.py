@@ -4,8 +4,13 @@ same seeded inputs.
 Bar (bf16 inputs, fp32 accumulation): over all compared output elements
 max |delta| <= 1e-2 and mean |delta| <= 1e-3, plus max |delta| <= 2e-2 * max|o|
 (outputs shrink like 1/sqrt(L), which makes the absolute bounds loose at long
-contexts); LSE within 1e-3; the cache write-back bit-exact; pool slots the
-batch does not own untouched (they hold NaN, so a stray read or write shows).
+contexts); the cache write-back bit-exact; pool slots the batch does not own
+untouched (they hold NaN, so a stray read or write shows).
+
+LSE bound, derived from the arithmetic: the kernel rounds each softmax weight
+p_j to bf16 (RNE, relative error <= 2^-9) and sums the rounded values, so the
+row sum l carries a relative error <= 2^-9 and ln l an absolute error <=
+ln(1 + 2^-9) = 1.95e-3; fp32 score rounding adds ~1e-6. Bar: 2e-3.
 """
 import numpy as np
 import pytest
@@ -16,7 +21,7 @@ from oracle import oracle
 
 pytestmark = pytest.mark.gpu
 
-MAX_ABS, MEAN_ABS, REL_MAX, LSE_ABS = 1e-2, 1e-3, 2e-2, 1e-3
+MAX_ABS, MEAN_ABS, REL_MAX, LSE_ABS = 1e-2, 1e-3, 2e-2, 2e-3
 
 
 @pytest.fixture(scope="module")
@@ -43,14 +48,14 @@ def run(wl, dev, force_splits=0, fill=float("nan"), want_lse=True):
     return p, t, out, lse
 
 
-def compare(tag, got, ref, got_lse=None, ref_lse=None):
+def compare(tag, got, ref, got_lse=None, ref_lse=None, max_abs=None, mean_abs=MEAN_ABS):
     got = np.asarray(got, np.float64)
     assert np.isfinite(got).all(), f"{tag}: non-finite output"
     d = np.abs(got - ref)
     mx, mean = d.max(), d.mean()
-    bound = min(MAX_ABS, REL_MAX * np.abs(ref).max())
+    bound = min(MAX_ABS, REL_MAX * np.abs(ref).max()) if max_abs is None else max_abs
     assert mx <= bound, f"{tag}: max |delta| {mx:.3e} > {bound:.3e}"
-    assert mean <= MEAN_ABS, f"{tag}: mean |delta| {mean:.3e}"
+    assert mean <= mean_abs, f"{tag}: mean |delta| {mean:.3e} > {mean_abs:.3e}"
     if got_lse is not None:
         dl = np.abs(np.asarray(got_lse, np.float64) - ref_lse).max()
         assert dl <= LSE_ABS, f"{tag}: lse max |delta| {dl:.3e}"
@@ -146,9 +151,20 @@ def test_split_count_independence(dev):
 
 
 def test_q_stress(dev):
+    """Q scaled by 4: a peaky softmax where few weights dominate, so the bf16
+    rounding of P does not average out. Derived bound: weights renormalised by
+    the same rounded sum err by <= 2 * 2^-9 relative, so |sum (w~ - w) v| <=
+    2^-8 max|V|, and the bf16 output adds <= 2^-9 |o|: |delta| <= 1.5 * 2^-8 *
+    max|V| (mean: the same with mean|V|)."""
     wl = workloads.ragged_small(2, hq=28, hkv=4, d=128, q_scale=4.0)
     p, t, out, lse = run(wl, dev)
-    check_full(wl, out, lse)
+    ref, ref_lse = oracle.attention_all(wl)
+    vmax = max(float(wl.packed_v_new().float().abs().max()),
+               max(float(wl.v_ctx(i).float().abs().max()) for i in range(wl.num_items)
+                   if not wl.is_prefill[i]))
+    vmean = float(wl.packed_v_new().float().abs().mean())
+    compare(wl.name, out.float().cpu().numpy(), ref, lse.cpu().numpy(), ref_lse,
+            max_abs=1.5 * 2 ** -8 * vmax, mean_abs=1.5 * 2 ** -8 * vmean)
 
 
 def test_no_lse(dev):
