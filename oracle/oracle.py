@@ -102,16 +102,10 @@ class Call:
                 _ptr(self.q), _ptr(self.k_new), _ptr(self.v_new), _ptr(self.k_ctx), _ptr(self.v_ctx))
 
 
-def attention(wl, items: Optional[Sequence[int]] = None,
-              rows: Optional[Dict[int, Iterable[int]]] = None,
-              heads: Optional[Sequence[int]] = None) -> Dict[int, Tuple[np.ndarray, np.ndarray, np.ndarray]]:
-    """fp64 attention for the chosen items.
-
-    rows: optional {item: local row indices}; default every row.
-    heads: optional list of query heads; default all.
-    Returns {item: (local_rows, out [len(rows), len(heads), D], lse [len(rows), len(heads)])}.
-    """
-    call = Call(wl, items)
+def selection(call: Call, rows: Optional[Dict[int, Iterable[int]]] = None,
+              heads: Optional[Sequence[int]] = None):
+    """(row, head) pair list of a call: per item its chosen local rows (default
+    all) and heads (default all). Returns (sel array, {item: (rows, base)}, heads)."""
     hq = call.hq
     hs = list(range(hq)) if heads is None else list(heads)
     sel, layout = [], {}
@@ -123,12 +117,31 @@ def attention(wl, items: Optional[Sequence[int]] = None,
             for h in hs:
                 sel.append((int(call.q_indptr[k]) + int(r)) * hq + h)
         layout[i] = (rr, base)
-    sel_a = np.asarray(sel, np.int64)
+    return np.asarray(sel, np.int64), layout, hs
+
+
+def run(call: Call, sel: np.ndarray) -> Tuple[np.ndarray, np.ndarray]:
+    """The C oracle over prepared arrays: out [len(sel), D], lse [len(sel)]."""
     out = np.empty((len(sel), call.d), np.float64)
     lse = np.empty((len(sel),), np.float64)
-    rc = lib().oracle_attn(*call.args(), _ptr(sel_a), len(sel), _ptr(out), _ptr(lse))
+    rc = lib().oracle_attn(*call.args(), _ptr(sel), len(sel), _ptr(out), _ptr(lse))
     if rc != 0:
         raise ValueError(f"oracle_attn rejected the call (code {rc})")
+    return out, lse
+
+
+def attention(wl, items: Optional[Sequence[int]] = None,
+              rows: Optional[Dict[int, Iterable[int]]] = None,
+              heads: Optional[Sequence[int]] = None) -> Dict[int, Tuple[np.ndarray, np.ndarray, np.ndarray]]:
+    """fp64 attention for the chosen items.
+
+    rows: optional {item: local row indices}; default every row.
+    heads: optional list of query heads; default all.
+    Returns {item: (local_rows, out [len(rows), len(heads), D], lse [len(rows), len(heads)])}.
+    """
+    call = Call(wl, items)
+    sel, layout, hs = selection(call, rows, heads)
+    out, lse = run(call, sel)
     res = {}
     for i, (rr, base) in layout.items():
         cnt = len(rr) * len(hs)
