@@ -41,6 +41,7 @@ namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
@@ -79,12 +80,32 @@ __device__ __forceinline__ int swz_v(int r) {
     return D == 128 ? ((r & 3) << 2) : (((r >> 1) & 1) << 2);
 }
 
-__device__ __forceinline__ float bf16_bits_to_float(uint16_t b) {
-    return __uint_as_float(uint32_t(b) << 16);
+// Cross-half (lane l <-> l ^ 32) pair of a value: v_permlane32_swap with both
+// operands x returns (x[l], x[l^32]) for the lower half and (x[l^32], x[l])
+// for the upper half, so a symmetric combine of the two results is the pair's.
+__device__ __forceinline__ float half_max(float x) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float half_sum(float x) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
-template <int D, int QW, int KW, int NB, bool HEADS_ACROSS>
-__global__ __launch_bounds__(64 * QW * KW) void attn_tiles_kernel(AttnArgs a) {
+// The running max moves only when a score exceeds it by more than this (log2
+// units), so P <= 2^8 and O is rescaled rarely; the result is unchanged
+// because O and l always share the same reference.
+constexpr float kRescaleThreshold = 8.0f;
+
+// Work-groups per CU the register budget is sized for: two waves per SIMD for
+// four-wave work-groups whose staging fits twice in LDS.
+template <int D, int QW, int KW, int NB>
+constexpr int min_blocks_per_cu() {
+    return (QW * KW == 4 && 4 * (32 * NB * KW) * D * 2 <= 80 * 1024) ? 2 : 1;
+}
+
+template <int D, int QW, int KW, int NB, bool HEADS_ACROSS, int MINB>
+__global__ __launch_bounds__(64 * QW * KW, MINB) void attn_tiles_kernel(AttnArgs a) {
     constexpr int NT = 64 * QW * KW;     // threads
     constexpr int KT = 32 * NB;          // keys per wave per stage
     constexpr int STEP = KT * KW;        // keys per stage
@@ -99,8 +120,10 @@ __global__ __launch_bounds__(64 * QW * KW) void attn_tiles_kernel(AttnArgs a) {
     constexpr int MERGE_REGS = MB * 16 + 2;
     static_assert(KW == 1 || (QW * (KW - 1) * MERGE_REGS * 64 * 4) <= 4 * TILE,
                   "cross-wave merge must fit in the stage buffers");
+    constexpr int MAX_PAGES = kMaxCachedRange / 16;
 
     __shared__ __attribute__((aligned(1024))) uint8_t smem[4 * TILE];
+    __shared__ int32_t pages[MAX_PAGES];
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -115,6 +138,16 @@ __global__ __launch_bounds__(64 * QW * KW) void attn_tiles_kernel(AttnArgs a) {
     const int head = HEADS_ACROSS ? t.q_head0 + qs : t.q_head0;
     const int row = (HEADS_ACROSS ? t.row0 : t.row0 + 32 * qs) + qn;
     const bool row_ok = row < it.n;
+    const int kv_begin = t.kv_begin, kv_end = t.kv_end;
+    const int nstages = (kv_end - kv_begin + STEP - 1) / STEP;
+    // a whole prefill brings every position fresh: no page lookups
+    const bool all_fresh = it.o == 0 && it.n == it.L;
+    const int pg0 = kv_begin >> 4;
+    if (!all_fresh) {
+        // the tile's page ids, once (the plan keeps such ranges <= kMaxCachedRange)
+        const int npg = ((kv_end + 15) >> 4) - pg0;
+        for (int k = tid; k < npg; k += NT) pages[k] = a.page_ids[it.page_start + pg0 + k];
+    }
 
     // ---- Q fragments (B operand: k = dims, n = query), zero for rows past n
     bf16x8 qf[DS];
@@ -128,14 +161,49 @@ __global__ __launch_bounds__(64 * QW * KW) void attn_tiles_kernel(AttnArgs a) {
         }
     }
 
-    const int kv_begin = t.kv_begin, kv_end = t.kv_end;
-    const int nstages = (kv_end - kv_begin + STEP - 1) / STEP;
+    // ---- stage-invariant staging offsets: thread chunk j of a stage is key
+    // row r_j, source chunk (pos ^ swizzle(r_j)) of K and of V
+    const size_t row_stride = (size_t)a.hkv * D;                       // elements between positions
+    const uint16_t* kfresh = a.k_new + ((size_t)(it.q_start - it.o) * a.hkv + t.kv_head) * D;
+    const uint16_t* vfresh = a.v_new + ((size_t)(it.q_start - it.o) * a.hkv + t.kv_head) * D;
+    const size_t page_stride = (size_t)a.hkv * 16 * D;
+    const uint16_t* kcache = a.k_cache + (size_t)t.kv_head * 16 * D;
+    const uint16_t* vcache = a.v_cache + (size_t)t.kv_head * 16 * D;
 
-    // ---- stage loader: every thread moves NJ 16-byte chunks of K and of V
+    // per-thread byte offsets of its chunks within a stage of fresh rows
+    // (whole prefills): key row r_j at row_stride, swizzled chunk
+    uint32_t foff_k[NJ], foff_v[NJ];
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) {
+        const int P = j * NT + tid;
+        const int r = P / NC;
+        const int pos = P % NC;
+        foff_k[j] = uint32_t(r * row_stride * 2 + ((pos ^ swz_k<D>(r)) << 4));
+        foff_v[j] = uint32_t(r * row_stride * 2 + ((pos ^ swz_v<D>(r)) << 4));
+    }
+
     auto issue_stage = [&](int st, int buf) {
         uint8_t* kb = smem + buf * 2 * TILE;
         uint8_t* vb = kb + TILE;
         const int key0 = kv_begin + st * STEP;
+        const bool tail = key0 + STEP > kv_end;
+        if (all_fresh && !tail) {
+            // uniform base + precomputed 32-bit offsets
+            // (the builtin's source must stay a pointer to the element type:
+            // a byte pointer there makes hipcc drop every kernel's host stub)
+            const uint8_t* kbase = reinterpret_cast<const uint8_t*>(kfresh + (size_t)key0 * row_stride);
+            const uint8_t* vbase = reinterpret_cast<const uint8_t*>(vfresh + (size_t)key0 * row_stride);
+#pragma unroll
+            for (int j = 0; j < NJ; ++j) {
+                if ((NCH % NT) != 0 && j * NT + wave * 64 >= NCH) break;  // wave-uniform
+                const int dst = (j * NT + wave * 64) * 16;
+                __builtin_amdgcn_global_load_lds(reinterpret_cast<const uint16_t*>(kbase + foff_k[j]),
+                                                 (LDS void*)(kb + dst), 16, 0, 0);
+                __builtin_amdgcn_global_load_lds(reinterpret_cast<const uint16_t*>(vbase + foff_v[j]),
+                                                 (LDS void*)(vb + dst), 16, 0, 0);
+            }
+            return;
+        }
 #pragma unroll
         for (int j = 0; j < NJ; ++j) {
             if ((NCH % NT) != 0 && j * NT + wave * 64 >= NCH) break;  // wave-uniform
@@ -143,46 +211,58 @@ __global__ __launch_bounds__(64 * QW * KW) void attn_tiles_kernel(AttnArgs a) {
             const int r = P / NC;
             const int pos = P % NC;
             int p = key0 + r;
-            p = p < kv_end ? p : kv_begin;  // past the range: a valid row, masked later
-            const unsigned rel = unsigned(p - it.o);
-            size_t off;
-            const uint16_t *kbase, *vbase;
-            if (rel < unsigned(it.n)) {
-                off = ((size_t)(it.q_start + rel) * a.hkv + t.kv_head) * D;
-                kbase = a.k_new;
-                vbase = a.v_new;
+            if (tail) p = p < kv_end ? p : kv_begin;  // past the range: a valid row, masked later
+            const int ck = (pos ^ swz_k<D>(r)) * 8;
+            const int cv = (pos ^ swz_v<D>(r)) * 8;
+            const uint16_t *ksrc, *vsrc;
+            if (all_fresh || unsigned(p - it.o) < unsigned(it.n)) {
+                ksrc = kfresh + (size_t)p * row_stride;
+                vsrc = vfresh + (size_t)p * row_stride;
             } else {
-                const int page = a.page_ids[it.page_start + (p >> 4)];
-                off = (((size_t)page * a.hkv + t.kv_head) * 16 + (p & 15)) * D;
-                kbase = a.k_cache;
-                vbase = a.v_cache;
+                const size_t off = (size_t)pages[(p >> 4) - pg0] * page_stride + (p & 15) * D;
+                ksrc = kcache + off;
+                vsrc = vcache + off;
             }
-            const int ck = pos ^ swz_k<D>(r);
-            const int cv = pos ^ swz_v<D>(r);
             const int dst = (j * NT + wave * 64) * 16;
-            __builtin_amdgcn_global_load_lds(kbase + off + ck * 8, (LDS void*)(kb + dst), 16, 0, 0);
-            __builtin_amdgcn_global_load_lds(vbase + off + cv * 8, (LDS void*)(vb + dst), 16, 0, 0);
+            __builtin_amdgcn_global_load_lds(ksrc + ck, (LDS void*)(kb + dst), 16, 0, 0);
+            __builtin_amdgcn_global_load_lds(vsrc + cv, (LDS void*)(vb + dst), 16, 0, 0);
         }
     };
+
+    // ---- stage-invariant LDS read offsets
+    // K (A operand): lane reads key qn of each 32-key block, chunk 2k + hh
+    int koff[DS];
+#pragma unroll
+    for (int k = 0; k < DS; ++k) koff[k] = qn * ROWB + (((2 * k + hh) ^ swz_k<D>(qn)) << 4);
+    // V^T (A operand) via transposing reads: 16-lane group g16 covers dims
+    // mb*32 + (g16&1)*16 .. +15; lane (r4, j4) points at key row 4hh + r4 (+8),
+    // dims 4 j4 .. 4 j4 + 3 of that group
+    const int g16 = lane >> 4;
+    const int r4 = (lane >> 2) & 3;
+    const int j4 = lane & 3;
+    const int vrow = (4 * hh + r4) * ROWB;
+    int voff[MB];
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb) {
+        const int dim = mb * 32 + (g16 & 1) * 16 + 4 * j4;
+        voff[mb] = vrow + (((dim >> 3) ^ swz_v<D>(4 * hh + r4)) << 4) + (dim & 7) * 2;
+    }
 
     f32x16 o[MB];
 #pragma unroll
     for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
         for (int i = 0; i < 16; ++i) o[mb][i] = 0.0f;
-    float m_run = -INFINITY;  // running max (log2 domain) of this lane's query
-    float l_run = 0.0f;       // running sum over this lane's half of the keys
+    float m_used = -INFINITY;  // reference max (log2 domain) of this lane's query
+    float l_run = 0.0f;        // sum of rounded P over this lane's half of the keys
+    const float c = a.scale_log2;
 
-    issue_stage(0, 0);
-    for (int st = 0; st < nstages; ++st) {
-        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-        __syncthreads();
-        if (st + 1 < nstages) issue_stage(st + 1, (st + 1) & 1);
-
-        const uint8_t* kb = smem + (st & 1) * 2 * TILE;
-        const uint8_t* vb = kb + TILE;
-        const int sub0 = ks * KT;                         // wave's first key in the stage
-        const int key0 = kv_begin + st * STEP + sub0;     // its context position
+    if (!all_fresh) __syncthreads();  // page ids visible before the first loads
+    // tail: the stage may hold keys past the range (the last stage only)
+    auto compute_stage = [&](int st, bool tail) {
+        const uint8_t* kb = smem + (st & 1) * 2 * TILE + ks * KT * ROWB;
+        const uint8_t* vb = smem + (st & 1) * 2 * TILE + TILE + ks * KT * ROWB;
+        const int key0 = kv_begin + st * STEP + ks * KT;  // this wave's first key
 
         // S^T = K Q^T: rows = keys, columns = queries
         f32x16 s[NB];
@@ -190,70 +270,82 @@ __global__ __launch_bounds__(64 * QW * KW) void attn_tiles_kernel(AttnArgs a) {
         for (int b = 0; b < NB; ++b) {
 #pragma unroll
             for (int i = 0; i < 16; ++i) s[b][i] = 0.0f;
-            const int r = sub0 + b * 32 + qn;
 #pragma unroll
             for (int k = 0; k < DS; ++k) {
-                const int c = 2 * k + hh;
-                const bf16x8 kf = *(const LDS bf16x8*)(kb + r * ROWB + ((c ^ swz_k<D>(r)) << 4));
+                const bf16x8 kf = *(const LDS bf16x8*)(kb + b * 32 * ROWB + koff[k]);
                 s[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[k], s[b], 0, 0, 0);
             }
         }
+        if (tail) {
+#pragma unroll
+            for (int b = 0; b < NB; ++b)
+#pragma unroll
+                for (int i = 0; i < 16; ++i) {
+                    const int key = key0 + b * 32 + 8 * (i >> 2) + 4 * hh + (i & 3);
+                    if (key >= kv_end) s[b][i] = -INFINITY;
+                }
+        }
 
-        // online softmax (exp2 domain); keys past the range get -inf
+        // online softmax, exp2 domain, lazily rescaled
         float mx = -INFINITY;
 #pragma unroll
         for (int b = 0; b < NB; ++b)
 #pragma unroll
-            for (int i = 0; i < 16; ++i) {
-                const int key = key0 + b * 32 + 8 * (i >> 2) + 4 * hh + (i & 3);
-                const float v = key < kv_end ? s[b][i] * a.scale_log2 : -INFINITY;
-                s[b][i] = v;
-                mx = fmaxf(mx, v);
-            }
-        mx = fmaxf(mx, __shfl_xor(mx, 32));
-        const float m_new = fmaxf(m_run, mx);
-        const float m_ref = m_new == -INFINITY ? 0.0f : m_new;
-        const float alpha = __builtin_amdgcn_exp2f(m_run - m_ref);
-        m_run = m_new;
-        l_run *= alpha;
+            for (int i = 0; i < 16; ++i) mx = fmaxf(mx, s[b][i]);
+        const float mx_s = half_max(mx) * c;
+        const bool need = mx_s > m_used + kRescaleThreshold;
+        if (__builtin_amdgcn_ballot_w64(need)) {
+            const float alpha = need ? __builtin_amdgcn_exp2f(m_used - mx_s) : 1.0f;
+            m_used = need ? mx_s : m_used;
+            l_run *= alpha;
 #pragma unroll
-        for (int mb = 0; mb < MB; ++mb)
+            for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
-            for (int i = 0; i < 16; ++i) o[mb][i] *= alpha;
+                for (int i = 0; i < 16; ++i) o[mb][i] *= alpha;
+        }
+        const float mref = m_used == -INFINITY ? 0.0f : m_used;
 
         bf16x8 pf[NB][2];
 #pragma unroll
         for (int b = 0; b < NB; ++b)
 #pragma unroll
-            for (int i = 0; i < 16; ++i) {
-                const __bf16 pb = (__bf16)__builtin_amdgcn_exp2f(s[b][i] - m_ref);
-                l_run += (float)pb;
-                pf[b][i >> 3][i & 7] = pb;
+            for (int i = 0; i < 16; i += 2) {
+                const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[b][i], c, -mref));
+                const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[b][i + 1], c, -mref));
+                const bf16x2 pp = {(__bf16)p0, (__bf16)p1};
+                l_run = __builtin_amdgcn_fdot2_f32_bf16(pp, bf16x2{(__bf16)1.0f, (__bf16)1.0f}, l_run, false);
+                pf[b][i >> 3][i & 7] = pp[0];
+                pf[b][i >> 3][(i & 7) + 1] = pp[1];
             }
 
         // O^T += V^T P^T; lane slot j of P^T holds key 16kk + 8(j/4) + 4hh + j%4
-        const int g16 = lane >> 4;
-        const int r4 = (lane >> 2) & 3;
-        const int j4 = lane & 3;
 #pragma unroll
         for (int b = 0; b < NB; ++b)
 #pragma unroll
-            for (int kk = 0; kk < 2; ++kk) {
-                const int ra = sub0 + b * 32 + kk * 16 + 4 * hh + r4;
-                const int rb = ra + 8;
+            for (int kk = 0; kk < 2; ++kk)
 #pragma unroll
                 for (int mb = 0; mb < MB; ++mb) {
-                    const int dim = mb * 32 + (g16 & 1) * 16 + 4 * j4;
-                    const int cb = dim >> 3;
-                    const int hb = (dim & 7) * 2;
-                    const bf16x4 va = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
-                        (LDS bf16x4*)(vb + ra * ROWB + ((cb ^ swz_v<D>(ra)) << 4) + hb));
-                    const bf16x4 vbv = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
-                        (LDS bf16x4*)(vb + rb * ROWB + ((cb ^ swz_v<D>(rb)) << 4) + hb));
-                    const bf16x8 vf = {va[0], va[1], va[2], va[3], vbv[0], vbv[1], vbv[2], vbv[3]};
+                    const uint8_t* vp = vb + (b * 32 + kk * 16) * ROWB + voff[mb];
+                    const bf16x4 va = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((LDS bf16x4*)(vp));
+                    const bf16x4 vc = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((LDS bf16x4*)(vp + 8 * ROWB));
+                    const bf16x8 vf = {va[0], va[1], va[2], va[3], vc[0], vc[1], vc[2], vc[3]};
                     o[mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[b][kk], o[mb], 0, 0, 0);
                 }
-            }
+    };
+
+    issue_stage(0, 0);
+    const int full_stages = (kv_end - kv_begin) / STEP;  // stages with no key past the range
+    int st = 0;
+    for (; st < full_stages; ++st) {
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        __syncthreads();
+        if (st + 1 < nstages) issue_stage(st + 1, (st + 1) & 1);
+        compute_stage(st, false);
+    }
+    if (st < nstages) {  // the last, partial stage
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        __syncthreads();
+        compute_stage(st, true);
     }
 
     // ---- combine the context sub-ranges of the waves that share query rows
@@ -266,18 +358,19 @@ __global__ __launch_bounds__(64 * QW * KW) void attn_tiles_kernel(AttnArgs a) {
             for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
                 for (int i = 0; i < 16; ++i) dst[(mb * 16 + i) * 64 + lane] = o[mb][i];
-            dst[(MB * 16) * 64 + lane] = m_run;
+            dst[(MB * 16) * 64 + lane] = m_used;
             dst[(MB * 16 + 1) * 64 + lane] = l_run;
         }
         __syncthreads();
         if (ks > 0) return;
-        float m_tot = m_run;
+        float m_tot = m_used;
 #pragma unroll
         for (int k = 1; k < KW; ++k) {
             const float* src = mbuf + (size_t)((qs * (KW - 1) + (k - 1)) * MERGE_REGS) * 64;
             m_tot = fmaxf(m_tot, src[(MB * 16) * 64 + lane]);
         }
-        const float sc0 = __builtin_amdgcn_exp2f(m_run - m_tot);
+        // wave ks = 0 always holds a valid key, so m_tot is finite
+        const float sc0 = __builtin_amdgcn_exp2f(m_used - m_tot);
         l_run *= sc0;
 #pragma unroll
         for (int mb = 0; mb < MB; ++mb)
@@ -293,13 +386,13 @@ __global__ __launch_bounds__(64 * QW * KW) void attn_tiles_kernel(AttnArgs a) {
 #pragma unroll
                 for (int i = 0; i < 16; ++i) o[mb][i] += sck * src[(mb * 16 + i) * 64 + lane];
         }
-        m_run = m_tot;
+        m_used = m_tot;
     }
 
     // ---- epilogue
-    const float l_tot = l_run + __shfl_xor(l_run, 32);
+    const float l_tot = half_sum(l_run);
     const float inv = 1.0f / l_tot;
-    const float lse_val = m_run * 0.69314718055994530942f + logf(l_tot);
+    const float lse_val = m_used * 0.69314718055994530942f + logf(l_tot);
     if (!row_ok) return;
     if (it.num_splits > 1) {
         const size_t prow = (size_t)(t.split * it.n + row) * a.hq + head;
@@ -412,7 +505,8 @@ __global__ __launch_bounds__(256) void merge_kernel(MergeArgs a) {
 // ------------------------------------------------------------------ launch
 template <int D, int QW, int KW, int NB, bool HA>
 hipError_t launch_tiles(const AttnArgs& args, int n_tiles, hipStream_t stream) {
-    attn_tiles_kernel<D, QW, KW, NB, HA><<<dim3(n_tiles), dim3(64 * QW * KW), 0, stream>>>(args);
+    constexpr int MINB = min_blocks_per_cu<D, QW, KW, NB>();
+    attn_tiles_kernel<D, QW, KW, NB, HA, MINB><<<dim3(n_tiles), dim3(64 * QW * KW), 0, stream>>>(args);
     return hipGetLastError();
 }
 

@@ -170,6 +170,10 @@ extern "C" sangam_status sangam_attn_plan(const sangam_attn_desc* d, void* plan_
         } else {
             S = 1;
         }
+        // a tile that reads cached rows stages its page ids in LDS, which
+        // bounds its context range
+        const bool all_fresh = it.o == 0 && it.n == it.L;
+        if (!all_fresh) S = std::max<int64_t>(S, ceil_div(it.L, kMaxCachedRange));
         int64_t len = round_up(ceil_div(it.L, S), kKeyAlign);
         S = ceil_div(it.L, len);  // no empty chunk
         it.num_splits = int32_t(S);

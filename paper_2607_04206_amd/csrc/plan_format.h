@@ -16,6 +16,9 @@ constexpr int kPrefillQWaves = 4;   // waves of a prefill-shaped work-group
 constexpr int kPrefillRows = kWaveRows * kPrefillQWaves;
 constexpr int kKeyAlign = 64;       // split boundaries are multiples of this many keys
 constexpr int kForcedSplitLen = 8192;  // a decode context longer than this is always split
+// Longest context range of one tile that reads cached (paged) rows: the
+// kernel stages that range's page ids in LDS.
+constexpr int kMaxCachedRange = 8192;
 
 // One work item of the batch (a block decode or a whole prefill).
 struct ItemRec {

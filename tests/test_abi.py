@@ -95,3 +95,11 @@ def test_plan_info_and_workspace_query():
     assert _lib.lib.sangam_plan_workspace_bytes(junk.ctypes.data) == 0
     info = _lib.PlanInfo()
     assert _lib.lib.sangam_plan_get_info(junk.ctypes.data, ctypes.byref(info)) == -8
+
+
+def test_no_undefined_kernel_stubs():
+    # hipcc can silently omit host launch stubs for kernel templates; the
+    # library then fails to load with an undefined __device_stub__ symbol
+    out = subprocess.run(["nm", "-D", "--undefined-only", _lib.LIB_PATH], capture_output=True,
+                         text=True, check=True).stdout
+    assert "__device_stub__" not in out

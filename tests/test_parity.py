@@ -8,9 +8,10 @@ contexts); the cache write-back bit-exact; pool slots the batch does not own
 untouched (they hold NaN, so a stray read or write shows).
 
 LSE bound, derived from the arithmetic: the kernel rounds each softmax weight
-p_j to bf16 (RNE, relative error <= 2^-9) and sums the rounded values, so the
-row sum l carries a relative error <= 2^-9 and ln l an absolute error <=
-ln(1 + 2^-9) = 1.95e-3; fp32 score rounding adds ~1e-6. Bar: 2e-3.
+p_j to bf16 (8 significant bits, RNE: relative error <= 2^-8) and sums the
+rounded values, so the row sum l carries a relative error <= 2^-8 and ln l an
+absolute error <= -ln(1 - 2^-8) = 3.9e-3; fp32 score rounding adds ~1e-6.
+Bar: 4e-3.
 """
 import numpy as np
 import pytest
@@ -21,7 +22,7 @@ from oracle import oracle
 
 pytestmark = pytest.mark.gpu
 
-MAX_ABS, MEAN_ABS, REL_MAX, LSE_ABS = 1e-2, 1e-3, 2e-2, 2e-3
+MAX_ABS, MEAN_ABS, REL_MAX, LSE_ABS = 1e-2, 1e-3, 2e-2, 4e-3
 
 
 @pytest.fixture(scope="module")
@@ -152,10 +153,11 @@ def test_split_count_independence(dev):
 
 def test_q_stress(dev):
     """Q scaled by 4: a peaky softmax where few weights dominate, so the bf16
-    rounding of P does not average out. Derived bound: weights renormalised by
-    the same rounded sum err by <= 2 * 2^-9 relative, so |sum (w~ - w) v| <=
-    2^-8 max|V|, and the bf16 output adds <= 2^-9 |o|: |delta| <= 1.5 * 2^-8 *
-    max|V| (mean: the same with mean|V|)."""
+    rounding of P does not average out. Derived bound: each weight is rounded
+    to bf16 (relative error <= 2^-8) and renormalised by the same rounded sum,
+    so it errs by <= 2 * 2^-8 relative and |sum (w~ - w) v| <= 2^-7 max|V|;
+    the bf16 output adds <= 2^-8 |o|: |delta| <= 1.5 * 2^-7 * max|V| (mean:
+    the same with mean|V|)."""
     wl = workloads.ragged_small(2, hq=28, hkv=4, d=128, q_scale=4.0)
     p, t, out, lse = run(wl, dev)
     ref, ref_lse = oracle.attention_all(wl)
@@ -164,7 +166,7 @@ def test_q_stress(dev):
                    if not wl.is_prefill[i]))
     vmean = float(wl.packed_v_new().float().abs().mean())
     compare(wl.name, out.float().cpu().numpy(), ref, lse.cpu().numpy(), ref_lse,
-            max_abs=1.5 * 2 ** -8 * vmax, mean_abs=1.5 * 2 ** -8 * vmean)
+            max_abs=1.5 * 2 ** -7 * vmax, mean_abs=1.5 * 2 ** -7 * vmean)
 
 
 def test_no_lse(dev):
