@@ -98,13 +98,24 @@ __device__ __forceinline__ float half_sum(float x) {
 constexpr float kRescaleThreshold = 8.0f;
 
 // Work-groups per CU the register budget is sized for: two waves per SIMD for
-// four-wave work-groups whose staging fits twice in LDS.
-template <int D, int QW, int KW, int NB>
+// four-wave work-groups whose staging fits twice in LDS and whose waves hold
+// one query block; one wave per SIMD otherwise.
+template <int D, int QW, int KW, int QB, int NB, int NSTAGE>
 constexpr int min_blocks_per_cu() {
-    return (QW * KW == 4 && 4 * (32 * NB * KW) * D * 2 <= 80 * 1024) ? 2 : 1;
+    return (QB == 1 && QW * KW == 4 && 2 * NSTAGE * (32 * NB * KW) * D * 2 <= 80 * 1024) ? 2 : 1;
 }
 
-template <int D, int QW, int KW, int NB, bool HEADS_ACROSS, int MINB>
+// One work-group per plan tile: a context range [kv_begin, kv_end) of one
+// item and KV head against QW query slots x QB blocks of 32 rows per slot.
+//   D      head dim (64, 128)
+//   QW     waves holding distinct query rows (query heads of a GQA group when
+//          HEADS_ACROSS, else consecutive 32*QB-row blocks of one head)
+//   KW     waves splitting each stage's keys (merged through LDS at the end)
+//   QB     32-row query blocks per wave: every K and V fragment read from
+//          LDS feeds QB MFMAs, so QB = 2 halves LDS traffic per flop
+//   NB     32-key blocks per wave per stage
+//   NSTAGE K/V stage buffers in LDS (NSTAGE - 1 stages in flight)
+template <int D, int QW, int KW, int QB, int NB, int NSTAGE, bool HEADS_ACROSS, int MINB>
 __global__ __launch_bounds__(64 * QW * KW, MINB) void attn_tiles_kernel(AttnArgs a) {
     constexpr int NT = 64 * QW * KW;     // threads
     constexpr int KT = 32 * NB;          // keys per wave per stage
@@ -118,11 +129,17 @@ __global__ __launch_bounds__(64 * QW * KW, MINB) void attn_tiles_kernel(AttnArgs
     constexpr int MB = D / 32;           // 32-dim blocks of O^T
     static_assert(NCH % 64 == 0, "a wave moves whole 1 KiB rows of chunks");
     constexpr int MERGE_REGS = MB * 16 + 2;
-    static_assert(KW == 1 || (QW * (KW - 1) * MERGE_REGS * 64 * 4) <= 4 * TILE,
+    static_assert(KW == 1 || QB == 1, "context-splitting waves hold one query block");
+    static_assert(!HEADS_ACROSS || QB == 1, "a decode block is 32 rows");
+    static_assert(KW == 1 || (QW * (KW - 1) * MERGE_REGS * 64 * 4) <= 2 * NSTAGE * TILE,
                   "cross-wave merge must fit in the stage buffers");
+    static_assert(NSTAGE >= 2 && NSTAGE <= 4, "2 to 4 stage buffers");
+    // with more than two buffers the wait counts loads, so every wave must
+    // issue the same number per stage
+    static_assert(NSTAGE == 2 || NCH % NT == 0, "deeper pipelines need whole staging rounds");
     constexpr int MAX_PAGES = kMaxCachedRange / 16;
 
-    __shared__ __attribute__((aligned(1024))) uint8_t smem[4 * TILE];
+    __shared__ __attribute__((aligned(1024))) uint8_t smem[2 * NSTAGE * TILE];
     __shared__ int32_t pages[MAX_PAGES];
 
     const int tid = threadIdx.x;
@@ -130,14 +147,13 @@ __global__ __launch_bounds__(64 * QW * KW, MINB) void attn_tiles_kernel(AttnArgs
     const int wave = uniform(tid >> 6);
     const int qs = wave % QW;
     const int ks = wave / QW;
-    const int qn = lane & 31;   // query (column) this lane holds
+    const int qn = lane & 31;   // query (column) this lane holds in each block
     const int hh = lane >> 5;   // half-wave
 
     const TileRec t = a.tiles[blockIdx.x];
     const ItemRec it = a.items[t.item];
     const int head = HEADS_ACROSS ? t.q_head0 + qs : t.q_head0;
-    const int row = (HEADS_ACROSS ? t.row0 : t.row0 + 32 * qs) + qn;
-    const bool row_ok = row < it.n;
+    const int row_base = HEADS_ACROSS ? t.row0 : t.row0 + 32 * QB * qs;
     const int kv_begin = t.kv_begin, kv_end = t.kv_end;
     const int nstages = (kv_end - kv_begin + STEP - 1) / STEP;
     // a whole prefill brings every position fresh: no page lookups
@@ -150,14 +166,17 @@ __global__ __launch_bounds__(64 * QW * KW, MINB) void attn_tiles_kernel(AttnArgs
     }
 
     // ---- Q fragments (B operand: k = dims, n = query), zero for rows past n
-    bf16x8 qf[DS];
-    {
-        const uint16_t* qp = a.q + ((size_t)(it.q_start + (row_ok ? row : 0)) * a.hq + head) * D;
+    bf16x8 qf[QB][DS];
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb) {
+        const int row = row_base + 32 * qb + qn;
+        const bool ok = row < it.n;
+        const uint16_t* qp = a.q + ((size_t)(it.q_start + (ok ? row : 0)) * a.hq + head) * D;
 #pragma unroll
         for (int s = 0; s < DS; ++s) {
             u32x4 v = *(const u32x4*)(qp + 16 * s + 8 * hh);
-            if (!row_ok) v = u32x4{0, 0, 0, 0};
-            qf[s] = __builtin_bit_cast(bf16x8, v);
+            if (!ok) v = u32x4{0, 0, 0, 0};
+            qf[qb][s] = __builtin_bit_cast(bf16x8, v);
         }
     }
 
@@ -248,77 +267,107 @@ __global__ __launch_bounds__(64 * QW * KW, MINB) void attn_tiles_kernel(AttnArgs
         voff[mb] = vrow + (((dim >> 3) ^ swz_v<D>(4 * hh + r4)) << 4) + (dim & 7) * 2;
     }
 
-    f32x16 o[MB];
+    f32x16 o[QB][MB];
+    float m_used[QB];  // reference max (log2 domain) of this lane's query, per block
+    float l_run[QB];   // sum of rounded P over this lane's half of the keys
 #pragma unroll
-    for (int mb = 0; mb < MB; ++mb)
+    for (int qb = 0; qb < QB; ++qb) {
+        m_used[qb] = -INFINITY;
+        l_run[qb] = 0.0f;
 #pragma unroll
-        for (int i = 0; i < 16; ++i) o[mb][i] = 0.0f;
-    float m_used = -INFINITY;  // reference max (log2 domain) of this lane's query
-    float l_run = 0.0f;        // sum of rounded P over this lane's half of the keys
+        for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+            for (int i = 0; i < 16; ++i) o[qb][mb][i] = 0.0f;
+    }
     const float c = a.scale_log2;
 
     if (!all_fresh) __syncthreads();  // page ids visible before the first loads
-    // tail: the stage may hold keys past the range (the last stage only)
-    auto compute_stage = [&](int st, bool tail) {
-        const uint8_t* kb = smem + (st & 1) * 2 * TILE + ks * KT * ROWB;
-        const uint8_t* vb = smem + (st & 1) * 2 * TILE + TILE + ks * KT * ROWB;
-        const int key0 = kv_begin + st * STEP + ks * KT;  // this wave's first key
 
-        // S^T = K Q^T: rows = keys, columns = queries
-        f32x16 s[NB];
+    // S^T = K Q^T for this wave's NB 32-key blocks of stage st: rows = keys,
+    // columns = queries; each K fragment feeds the QB query blocks
+    auto qk = [&](int st, f32x16 (&s)[QB][NB]) {
+        const uint8_t* kb = smem + (st % NSTAGE) * 2 * TILE + ks * KT * ROWB;
 #pragma unroll
         for (int b = 0; b < NB; ++b) {
 #pragma unroll
-            for (int i = 0; i < 16; ++i) s[b][i] = 0.0f;
+            for (int qb = 0; qb < QB; ++qb)
+#pragma unroll
+                for (int i = 0; i < 16; ++i) s[qb][b][i] = 0.0f;
 #pragma unroll
             for (int k = 0; k < DS; ++k) {
                 const bf16x8 kf = *(const LDS bf16x8*)(kb + b * 32 * ROWB + koff[k]);
-                s[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[k], s[b], 0, 0, 0);
+#pragma unroll
+                for (int qb = 0; qb < QB; ++qb)
+                    s[qb][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[qb][k], s[qb][b], 0, 0, 0);
             }
         }
+    };
+
+    // Online softmax of stage st's scores (exp2 domain) and O^T += V^T P^T.
+    // The reference max moves (and O, l are rescaled) only when a score
+    // exceeds it by more than kRescaleThreshold, which is rare after the first
+    // stage. tail: the stage may hold keys past the range (set to -inf).
+    auto softmax_pv = [&](int st, f32x16 (&s)[QB][NB], bool tail) {
+        const uint8_t* vb = smem + (st % NSTAGE) * 2 * TILE + TILE + ks * KT * ROWB;
         if (tail) {
+            const int key0 = kv_begin + st * STEP + ks * KT;  // this wave's first key
 #pragma unroll
             for (int b = 0; b < NB; ++b)
 #pragma unroll
                 for (int i = 0; i < 16; ++i) {
                     const int key = key0 + b * 32 + 8 * (i >> 2) + 4 * hh + (i & 3);
-                    if (key >= kv_end) s[b][i] = -INFINITY;
+#pragma unroll
+                    for (int qb = 0; qb < QB; ++qb)
+                        if (key >= kv_end) s[qb][b][i] = -INFINITY;
+                }
+        }
+        float mx_s[QB];
+        bool any_need = false;
+#pragma unroll
+        for (int qb = 0; qb < QB; ++qb) {
+            float mx = -INFINITY;
+#pragma unroll
+            for (int b = 0; b < NB; ++b)
+#pragma unroll
+                for (int i = 0; i < 16; ++i) mx = fmaxf(mx, s[qb][b][i]);
+            mx_s[qb] = half_max(mx) * c;
+            any_need |= mx_s[qb] > m_used[qb] + kRescaleThreshold;
+        }
+        if (__builtin_amdgcn_ballot_w64(any_need)) {
+#pragma unroll
+            for (int qb = 0; qb < QB; ++qb) {
+                const bool need = mx_s[qb] > m_used[qb] + kRescaleThreshold;
+                const float alpha = need ? __builtin_amdgcn_exp2f(m_used[qb] - mx_s[qb]) : 1.0f;
+                m_used[qb] = need ? mx_s[qb] : m_used[qb];
+                l_run[qb] *= alpha;
+#pragma unroll
+                for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+                    for (int i = 0; i < 16; ++i) o[qb][mb][i] *= alpha;
+            }
+        }
+
+        // P = exp2(s c - m) rounded to bf16 (the PV operand); l += the rounded values
+        bf16x8 pf[QB][NB][2];
+#pragma unroll
+        for (int qb = 0; qb < QB; ++qb) {
+            const float mref = m_used[qb] == -INFINITY ? 0.0f : m_used[qb];
+#pragma unroll
+            for (int b = 0; b < NB; ++b)
+#pragma unroll
+                for (int i = 0; i < 16; i += 2) {
+                    const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[qb][b][i], c, -mref));
+                    const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[qb][b][i + 1], c, -mref));
+                    const bf16x2 pp = {(__bf16)p0, (__bf16)p1};
+                    l_run[qb] = __builtin_amdgcn_fdot2_f32_bf16(pp, bf16x2{(__bf16)1.0f, (__bf16)1.0f},
+                                                                l_run[qb], false);
+                    pf[qb][b][i >> 3][i & 7] = pp[0];
+                    pf[qb][b][i >> 3][(i & 7) + 1] = pp[1];
                 }
         }
 
-        // online softmax, exp2 domain, lazily rescaled
-        float mx = -INFINITY;
-#pragma unroll
-        for (int b = 0; b < NB; ++b)
-#pragma unroll
-            for (int i = 0; i < 16; ++i) mx = fmaxf(mx, s[b][i]);
-        const float mx_s = half_max(mx) * c;
-        const bool need = mx_s > m_used + kRescaleThreshold;
-        if (__builtin_amdgcn_ballot_w64(need)) {
-            const float alpha = need ? __builtin_amdgcn_exp2f(m_used - mx_s) : 1.0f;
-            m_used = need ? mx_s : m_used;
-            l_run *= alpha;
-#pragma unroll
-            for (int mb = 0; mb < MB; ++mb)
-#pragma unroll
-                for (int i = 0; i < 16; ++i) o[mb][i] *= alpha;
-        }
-        const float mref = m_used == -INFINITY ? 0.0f : m_used;
-
-        bf16x8 pf[NB][2];
-#pragma unroll
-        for (int b = 0; b < NB; ++b)
-#pragma unroll
-            for (int i = 0; i < 16; i += 2) {
-                const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[b][i], c, -mref));
-                const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[b][i + 1], c, -mref));
-                const bf16x2 pp = {(__bf16)p0, (__bf16)p1};
-                l_run = __builtin_amdgcn_fdot2_f32_bf16(pp, bf16x2{(__bf16)1.0f, (__bf16)1.0f}, l_run, false);
-                pf[b][i >> 3][i & 7] = pp[0];
-                pf[b][i >> 3][(i & 7) + 1] = pp[1];
-            }
-
-        // O^T += V^T P^T; lane slot j of P^T holds key 16kk + 8(j/4) + 4hh + j%4
+        // lane slot j of P^T holds key 16kk + 8(j/4) + 4hh + j%4; each V
+        // fragment feeds the QB query blocks
 #pragma unroll
         for (int b = 0; b < NB; ++b)
 #pragma unroll
@@ -329,23 +378,42 @@ __global__ __launch_bounds__(64 * QW * KW, MINB) void attn_tiles_kernel(AttnArgs
                     const bf16x4 va = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((LDS bf16x4*)(vp));
                     const bf16x4 vc = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((LDS bf16x4*)(vp + 8 * ROWB));
                     const bf16x8 vf = {va[0], va[1], va[2], va[3], vc[0], vc[1], vc[2], vc[3]};
-                    o[mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[b][kk], o[mb], 0, 0, 0);
+#pragma unroll
+                    for (int qb = 0; qb < QB; ++qb)
+                        o[qb][mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[qb][b][kk], o[qb][mb], 0, 0, 0);
                 }
     };
 
-    issue_stage(0, 0);
+    // Stages st+1 .. st+NSTAGE-1 are in flight while stage st is computed.
+    // Loads complete in order, so waiting for stage st leaves the later
+    // stages outstanding.
+    constexpr int LPS = 2 * NJ;  // loads per stage per thread (K and V)
     const int full_stages = (kv_end - kv_begin) / STEP;  // stages with no key past the range
+    auto wait_stage = [&](int st) {
+        const int later = min(NSTAGE - 2, nstages - 1 - st);  // stages issued after st
+        if (NSTAGE >= 4 && later >= 2)
+            asm volatile("s_waitcnt vmcnt(%0)" ::"n"(2 * LPS) : "memory");
+        else if (NSTAGE >= 3 && later >= 1)
+            asm volatile("s_waitcnt vmcnt(%0)" ::"n"(LPS) : "memory");
+        else
+            asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    };
+    for (int k = 0; k < NSTAGE - 1 && k < nstages; ++k) issue_stage(k, k);
     int st = 0;
     for (; st < full_stages; ++st) {
-        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        wait_stage(st);
         __syncthreads();
-        if (st + 1 < nstages) issue_stage(st + 1, (st + 1) & 1);
-        compute_stage(st, false);
+        if (st + NSTAGE - 1 < nstages) issue_stage(st + NSTAGE - 1, (st + NSTAGE - 1) % NSTAGE);
+        f32x16 sc[QB][NB];
+        qk(st, sc);
+        softmax_pv(st, sc, false);
     }
     if (st < nstages) {  // the last, partial stage
         asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
         __syncthreads();
-        compute_stage(st, true);
+        f32x16 sc[QB][NB];
+        qk(st, sc);
+        softmax_pv(st, sc, true);
     }
 
     // ---- combine the context sub-ranges of the waves that share query rows
@@ -357,68 +425,73 @@ __global__ __launch_bounds__(64 * QW * KW, MINB) void attn_tiles_kernel(AttnArgs
 #pragma unroll
             for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
-                for (int i = 0; i < 16; ++i) dst[(mb * 16 + i) * 64 + lane] = o[mb][i];
-            dst[(MB * 16) * 64 + lane] = m_used;
-            dst[(MB * 16 + 1) * 64 + lane] = l_run;
+                for (int i = 0; i < 16; ++i) dst[(mb * 16 + i) * 64 + lane] = o[0][mb][i];
+            dst[(MB * 16) * 64 + lane] = m_used[0];
+            dst[(MB * 16 + 1) * 64 + lane] = l_run[0];
         }
         __syncthreads();
         if (ks > 0) return;
-        float m_tot = m_used;
+        float m_tot = m_used[0];
 #pragma unroll
         for (int k = 1; k < KW; ++k) {
             const float* src = mbuf + (size_t)((qs * (KW - 1) + (k - 1)) * MERGE_REGS) * 64;
             m_tot = fmaxf(m_tot, src[(MB * 16) * 64 + lane]);
         }
         // wave ks = 0 always holds a valid key, so m_tot is finite
-        const float sc0 = __builtin_amdgcn_exp2f(m_used - m_tot);
-        l_run *= sc0;
+        const float sc0 = __builtin_amdgcn_exp2f(m_used[0] - m_tot);
+        l_run[0] *= sc0;
 #pragma unroll
         for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
-            for (int i = 0; i < 16; ++i) o[mb][i] *= sc0;
+            for (int i = 0; i < 16; ++i) o[0][mb][i] *= sc0;
 #pragma unroll
         for (int k = 1; k < KW; ++k) {
             const float* src = mbuf + (size_t)((qs * (KW - 1) + (k - 1)) * MERGE_REGS) * 64;
             const float sck = __builtin_amdgcn_exp2f(src[(MB * 16) * 64 + lane] - m_tot);
-            l_run += sck * src[(MB * 16 + 1) * 64 + lane];
+            l_run[0] += sck * src[(MB * 16 + 1) * 64 + lane];
 #pragma unroll
             for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
-                for (int i = 0; i < 16; ++i) o[mb][i] += sck * src[(mb * 16 + i) * 64 + lane];
+                for (int i = 0; i < 16; ++i) o[0][mb][i] += sck * src[(mb * 16 + i) * 64 + lane];
         }
-        m_used = m_tot;
+        m_used[0] = m_tot;
     }
 
     // ---- epilogue
-    const float l_tot = half_sum(l_run);
-    const float inv = 1.0f / l_tot;
-    const float lse_val = m_used * 0.69314718055994530942f + logf(l_tot);
-    if (!row_ok) return;
-    if (it.num_splits > 1) {
-        const size_t prow = (size_t)(t.split * it.n + row) * a.hq + head;
-        float* po = a.ws + it.ws_o + prow * D;
 #pragma unroll
-        for (int mb = 0; mb < MB; ++mb)
+    for (int qb = 0; qb < QB; ++qb) {
+        const int row = row_base + 32 * qb + qn;
+        const float l_tot = half_sum(l_run[qb]);
+        const float inv = 1.0f / l_tot;
+        const float lse_val = m_used[qb] * 0.69314718055994530942f + logf(l_tot);
+        if (row >= it.n) continue;
+        if (it.num_splits > 1) {
+            const size_t prow = (size_t)(t.split * it.n + row) * a.hq + head;
+            float* po = a.ws + it.ws_o + prow * D;
 #pragma unroll
-            for (int q4 = 0; q4 < 4; ++q4) {
-                const int dim = mb * 32 + 8 * q4 + 4 * hh;
-                float4 v = {o[mb][4 * q4] * inv, o[mb][4 * q4 + 1] * inv, o[mb][4 * q4 + 2] * inv,
-                            o[mb][4 * q4 + 3] * inv};
-                *(float4*)(po + dim) = v;
-            }
-        if (hh == 0) a.ws[it.ws_lse + prow] = lse_val;
-    } else {
-        uint16_t* op = a.out + ((size_t)(it.q_start + row) * a.hq + head) * D;
+            for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
-        for (int mb = 0; mb < MB; ++mb)
+                for (int q4 = 0; q4 < 4; ++q4) {
+                    const int dim = mb * 32 + 8 * q4 + 4 * hh;
+                    float4 v = {o[qb][mb][4 * q4] * inv, o[qb][mb][4 * q4 + 1] * inv,
+                                o[qb][mb][4 * q4 + 2] * inv, o[qb][mb][4 * q4 + 3] * inv};
+                    *(float4*)(po + dim) = v;
+                }
+            if (hh == 0) a.ws[it.ws_lse + prow] = lse_val;
+        } else {
+            uint16_t* op = a.out + ((size_t)(it.q_start + row) * a.hq + head) * D;
 #pragma unroll
-            for (int q4 = 0; q4 < 4; ++q4) {
-                const int dim = mb * 32 + 8 * q4 + 4 * hh;
-                const bf16x4 v = {(__bf16)(o[mb][4 * q4] * inv), (__bf16)(o[mb][4 * q4 + 1] * inv),
-                                  (__bf16)(o[mb][4 * q4 + 2] * inv), (__bf16)(o[mb][4 * q4 + 3] * inv)};
-                *(u32x2*)(op + dim) = __builtin_bit_cast(u32x2, v);
-            }
-        if (hh == 0 && a.lse) a.lse[(size_t)(it.q_start + row) * a.hq + head] = lse_val;
+            for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+                for (int q4 = 0; q4 < 4; ++q4) {
+                    const int dim = mb * 32 + 8 * q4 + 4 * hh;
+                    const bf16x4 v = {(__bf16)(o[qb][mb][4 * q4] * inv), (__bf16)(o[qb][mb][4 * q4 + 1] * inv),
+                                      (__bf16)(o[qb][mb][4 * q4 + 2] * inv),
+                                      (__bf16)(o[qb][mb][4 * q4 + 3] * inv)};
+                    *(u32x2*)(op + dim) = __builtin_bit_cast(u32x2, v);
+                }
+            if (hh == 0 && a.lse) a.lse[(size_t)(it.q_start + row) * a.hq + head] = lse_val;
+        }
     }
 }
 
@@ -503,10 +576,11 @@ __global__ __launch_bounds__(256) void merge_kernel(MergeArgs a) {
 }
 
 // ------------------------------------------------------------------ launch
-template <int D, int QW, int KW, int NB, bool HA>
+template <int D, int QW, int KW, int QB, int NB, bool HA, int NSTAGE = 2>
 hipError_t launch_tiles(const AttnArgs& args, int n_tiles, hipStream_t stream) {
-    constexpr int MINB = min_blocks_per_cu<D, QW, KW, NB>();
-    attn_tiles_kernel<D, QW, KW, NB, HA, MINB><<<dim3(n_tiles), dim3(64 * QW * KW), 0, stream>>>(args);
+    constexpr int MINB = min_blocks_per_cu<D, QW, KW, QB, NB, NSTAGE>();
+    attn_tiles_kernel<D, QW, KW, QB, NB, NSTAGE, HA, MINB>
+        <<<dim3(n_tiles), dim3(64 * QW * KW), 0, stream>>>(args);
     return hipGetLastError();
 }
 
@@ -514,16 +588,16 @@ template <int D>
 hipError_t launch_decode(const AttnArgs& args, int n_tiles, int qw, int kw, int nb, hipStream_t stream,
                          bool* supported) {
     *supported = true;
-    if (qw == 1 && kw == 4 && nb == 1) return launch_tiles<D, 1, 4, 1, true>(args, n_tiles, stream);
-    if (qw == 2 && kw == 2 && nb == 2) return launch_tiles<D, 2, 2, 2, true>(args, n_tiles, stream);
+    if (qw == 1 && kw == 4 && nb == 1) return launch_tiles<D, 1, 4, 1, 1, true>(args, n_tiles, stream);
+    if (qw == 2 && kw == 2 && nb == 2) return launch_tiles<D, 2, 2, 1, 2, true>(args, n_tiles, stream);
     if (kw == 1 && nb == 2) {
         switch (qw) {
-            case 3: return launch_tiles<D, 3, 1, 2, true>(args, n_tiles, stream);
-            case 4: return launch_tiles<D, 4, 1, 2, true>(args, n_tiles, stream);
-            case 5: return launch_tiles<D, 5, 1, 2, true>(args, n_tiles, stream);
-            case 6: return launch_tiles<D, 6, 1, 2, true>(args, n_tiles, stream);
-            case 7: return launch_tiles<D, 7, 1, 2, true>(args, n_tiles, stream);
-            case 8: return launch_tiles<D, 8, 1, 2, true>(args, n_tiles, stream);
+            case 3: return launch_tiles<D, 3, 1, 1, 2, true>(args, n_tiles, stream);
+            case 4: return launch_tiles<D, 4, 1, 1, 2, true>(args, n_tiles, stream);
+            case 5: return launch_tiles<D, 5, 1, 1, 2, true>(args, n_tiles, stream);
+            case 6: return launch_tiles<D, 6, 1, 1, 2, true>(args, n_tiles, stream);
+            case 7: return launch_tiles<D, 7, 1, 1, 2, true>(args, n_tiles, stream);
+            case 8: return launch_tiles<D, 8, 1, 1, 2, true>(args, n_tiles, stream);
             default: break;
         }
     }
@@ -616,8 +690,8 @@ static sangam_status forward_impl(const void* plan_host, const void* plan_dev, c
     if (h->n_prefill_tiles > 0) {
         args.tiles = reinterpret_cast<const TileRec*>(pd + h->off_prefill_tiles);
         hipError_t e = h->d == 128
-                           ? launch_tiles<128, kPrefillQWaves, 1, 2, false>(args, h->n_prefill_tiles, stream)
-                           : launch_tiles<64, kPrefillQWaves, 1, 2, false>(args, h->n_prefill_tiles, stream);
+                           ? launch_tiles<128, kPrefillQWaves, 1, kPrefillQBlocks, 2, false>(args, h->n_prefill_tiles, stream)
+                           : launch_tiles<64, kPrefillQWaves, 1, kPrefillQBlocks, 2, false>(args, h->n_prefill_tiles, stream);
         if (e != hipSuccess) return hip_fail(e, "prefill attention launch");
     }
     if (hipError_t e = mark(2); e != hipSuccess) return hip_fail(e, "event record");

@@ -283,6 +283,7 @@ extern "C" sangam_status sangam_attn_plan(const sangam_attn_desc* d, void* plan_
     h.n_merge_rows = n_merge;
     h.num_split_items = n_split_items;
     h.max_splits = max_splits;
+    h.prefill_rows = kPrefillRows;
     h.workspace_bytes = ws_floats * int64_t(sizeof(float));
     h.off_items = off_items;
     h.off_decode_tiles = off_dec;

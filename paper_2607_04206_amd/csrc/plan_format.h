@@ -13,7 +13,8 @@ constexpr uint32_t kPlanVersion = 1;
 
 constexpr int kWaveRows = 32;       // query rows held by one wave (one decode block)
 constexpr int kPrefillQWaves = 4;   // waves of a prefill-shaped work-group
-constexpr int kPrefillRows = kWaveRows * kPrefillQWaves;
+constexpr int kPrefillQBlocks = 1;  // 32-row query blocks per prefill wave
+constexpr int kPrefillRows = kWaveRows * kPrefillQBlocks * kPrefillQWaves;
 constexpr int kKeyAlign = 64;       // split boundaries are multiples of this many keys
 constexpr int kForcedSplitLen = 8192;  // a decode context longer than this is always split
 // Longest context range of one tile that reads cached (paged) rows: the
@@ -82,7 +83,7 @@ struct PlanHeader {
     int32_t n_merge_rows;
     int32_t num_split_items;
     int32_t max_splits;
-    int32_t reserved0;
+    int32_t prefill_rows;  // query rows per prefill-shaped tile
     int64_t workspace_bytes;
 
     uint64_t off_items;

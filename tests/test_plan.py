@@ -17,7 +17,7 @@ HEADER = np.dtype([
     ("num_pool_pages", "<i8"), ("total_q", "<i8"), ("total_pages", "<i8"),
     ("n_decode_tiles", "<i4"), ("decode_qw", "<i4"), ("decode_kw", "<i4"), ("decode_nb", "<i4"),
     ("n_prefill_tiles", "<i4"), ("prefill_nb", "<i4"), ("n_merge_rows", "<i4"),
-    ("num_split_items", "<i4"), ("max_splits", "<i4"), ("reserved0", "<i4"),
+    ("num_split_items", "<i4"), ("max_splits", "<i4"), ("prefill_rows", "<i4"),
     ("workspace_bytes", "<i8"),
     ("off_items", "<u8"), ("off_decode_tiles", "<u8"), ("off_prefill_tiles", "<u8"), ("off_merge", "<u8"),
 ])
@@ -61,6 +61,7 @@ def coverage(wl, p):
     h, items, dec, pre, _ = parse(p)
     G = wl.num_q_heads // wl.num_kv_heads
     qw = int(h["decode_qw"])
+    rows = int(h["prefill_rows"])
     cover = {}
     for i in range(wl.num_items):
         cover[i] = np.zeros((wl.num_q_heads, wl.n(i), int(wl.kv_len[i])), np.int32)
@@ -76,7 +77,7 @@ def coverage(wl, p):
         hd = int(t["q_head0"])
         assert hd // G == t["kv_head"]
         r0 = int(t["row0"])
-        cover[i][hd, r0:r0 + 128, t["kv_begin"]:t["kv_end"]] += 1
+        cover[i][hd, r0:r0 + rows, t["kv_begin"]:t["kv_end"]] += 1
     return cover
 
 
@@ -145,7 +146,8 @@ def test_longest_first():
     _, items, dec, pre, _ = parse(p)
     dc = dec["kv_end"] - dec["kv_begin"]
     assert np.all(np.diff(dc) <= 0)
-    rows = np.minimum(128, items["n"][pre["item"]] - pre["row0"])
+    h = parse(p)[0]
+    rows = np.minimum(int(h["prefill_rows"]), items["n"][pre["item"]] - pre["row0"])
     pc = (pre["kv_end"] - pre["kv_begin"]) * ((rows + 31) // 32)
     assert np.all(np.diff(pc) <= 0)
 
