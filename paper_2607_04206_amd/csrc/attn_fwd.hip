@@ -588,7 +588,7 @@ template <int D>
 hipError_t launch_decode(const AttnArgs& args, int n_tiles, int qw, int kw, int nb, hipStream_t stream,
                          bool* supported) {
     *supported = true;
-    if (qw == 1 && kw == 4 && nb == 1) return launch_tiles<D, 1, 4, 1, 1, true>(args, n_tiles, stream);
+    if (qw == 1 && kw == 2 && nb == 1) return launch_tiles<D, 1, 2, 1, 1, true>(args, n_tiles, stream);
     if (qw == 2 && kw == 2 && nb == 2) return launch_tiles<D, 2, 2, 1, 2, true>(args, n_tiles, stream);
     if (kw == 1 && nb == 2) {
         switch (qw) {

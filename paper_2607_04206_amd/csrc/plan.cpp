@@ -48,13 +48,19 @@ static int decode_q_waves(int group) {
     return 1;
 }
 
-// Context sub-range waves: keep at least four waves per work-group so that
-// enough loads are in flight per CU on the bandwidth-bound decode path.
+// Context sub-range waves of a decode work-group. MHA (one query head per
+// work-group) measured fastest with two context-splitting waves and two
+// work-groups per CU; pairs of query heads split two ways as well.
 static int decode_kv_waves(int qw) {
-    if (qw == 1) return 4;
-    if (qw == 2) return 2;
+    if (qw <= 2) return 2;
     return 1;
 }
+
+// Shortest context chunk the planner cuts for balance (forced splits above
+// kForcedSplitLen aside): a chunk must carry enough keys to amortize a
+// work-group's prologue and its merge traffic. A GQA work-group does G times
+// the work per key, so it tolerates shorter chunks.
+static int64_t min_chunk(int qw) { return qw == 1 ? 2048 : 512; }
 
 const PlanHeader* check_plan(const void* plan) {
     if (!plan) return nullptr;
@@ -149,7 +155,7 @@ extern "C" sangam_status sangam_attn_plan(const sangam_attn_desc* d, void* plan_
         if (n <= kWaveRows) decode_keys += int64_t(hkv) * tiles_per_kv_head * d->kv_len[i];
     }
     int64_t chunk = ceil_div(decode_keys, 4 * int64_t(num_cus));
-    chunk = std::min<int64_t>(std::max<int64_t>(round_up(std::max<int64_t>(chunk, 1), kKeyAlign), 512),
+    chunk = std::min<int64_t>(std::max<int64_t>(round_up(std::max<int64_t>(chunk, 1), kKeyAlign), min_chunk(qw)),
                               kForcedSplitLen);
 
     std::vector<ItemRec> items(n_items);
@@ -277,7 +283,7 @@ extern "C" sangam_status sangam_attn_plan(const sangam_attn_desc* d, void* plan_
     h.n_decode_tiles = int32_t(dec.size());
     h.decode_qw = qw;
     h.decode_kw = kw;
-    h.decode_nb = (kw >= 4) ? 1 : 2;
+    h.decode_nb = qw == 1 ? 1 : 2;
     h.n_prefill_tiles = int32_t(pre.size());
     h.prefill_nb = 2;
     h.n_merge_rows = n_merge;

@@ -160,8 +160,8 @@ def test_deterministic_bytes():
 
 
 def test_decode_wave_shapes():
-    for hq, hkv, qw, kw in [(32, 32, 1, 4), (8, 4, 2, 2), (28, 4, 7, 1), (24, 8, 3, 1),
-                            (16, 1, 8, 1), (18, 2, 3, 1), (11, 1, 1, 4)]:
+    for hq, hkv, qw, kw in [(32, 32, 1, 2), (8, 4, 2, 2), (28, 4, 7, 1), (24, 8, 3, 1),
+                            (16, 1, 8, 1), (18, 2, 3, 1), (11, 1, 1, 2)]:
         wl = workloads.make_workload("s", 0, hq=hq, hkv=hkv, d=128, decodes=[(0, 64)], prefills=[])
         p = plan_of(wl)
         assert (p.info.decode_q_waves, p.info.decode_kv_waves) == (qw, kw), (hq, hkv)
