@@ -7,6 +7,12 @@ inputs are already resident in HBM. Prints one JSON line (rank 0).
 
     python bench.py [--steps K] [--warmup W] [--workload NAME] [--seed S]
 
+Timing: a short untimed pass records events between all four phases (the
+phase breakdown); the timed region then runs K whole steps with events only
+around the dominant attention launch, whose average duration gives the
+roofline figure. ms_per_step is host wall time over the K steps, bracketed by
+device synchronisation.
+
 Work counts are algorithmic: F = sum 4 n L D Hq flops (QK^T and PV, no causal
 halving) and B = K/V read once per item + cache write of the fresh rows + Q
 read + O write + page ids + LSE write.
@@ -173,11 +179,13 @@ def main():
               t["page_ids"].data_ptr(), out.data_ptr(), lse.data_ptr(), ws.data_ptr(), ws.numel(),
               stream.cuda_stream]
 
-    def make_events():
-        evs = [torch.cuda.Event(enable_timing=True) for _ in range(5)]
+    def make_events(which=range(5)):
+        """Five event slots; slots outside `which` stay NULL (nothing recorded)."""
+        evs = [torch.cuda.Event(enable_timing=True) if j in which else None for j in range(5)]
         for e in evs:
-            e.record(stream)  # creates the HIP event
-        arr = (ctypes.c_void_p * 5)(*[e.cuda_event for e in evs])
+            if e is not None:
+                e.record(stream)  # creates the HIP event
+        arr = (ctypes.c_void_p * 5)(*[e.cuda_event if e is not None else None for e in evs])
         return evs, arr
 
     flush_buf = torch.empty((512 << 20,), dtype=torch.uint8, device=dev) if args.flush else None
@@ -194,16 +202,37 @@ def main():
     torch.cuda.synchronize()
     print(f"[bench] warmup done ({args.warmup} steps)", file=sys.stderr, flush=True)
 
+    # phase breakdown, outside the timed region: events between all four phases
     K = args.steps
-    evsets = [make_events() for _ in range(K)]
+    n_phase = max(3, min(K, 10))
+    evsets = [make_events() for _ in range(n_phase)]
+    torch.cuda.synchronize()
+    for k in range(n_phase):
+        if args.flush:
+            flush_buf.fill_(k & 0xFF)
+        check(lib.sangam_attn_forward_timed(*args_c, evsets[k][1]))
+    torch.cuda.synchronize()
+    phase_ms = {}
+    for j, name in enumerate(PHASES):
+        phase_ms[name] = float(np.mean([evsets[k][0][j].elapsed_time(evsets[k][0][j + 1])
+                                        for k in range(n_phase)]))
+    work = split_work(wl)
+    dom = max(("prefill_attn", "decode_attn"), key=lambda n: phase_ms[n] if work[n][0] > 0 else -1)
+    jd = PHASES.index(dom)
+
+    # timed region: K whole steps; only the dominant kernel is bracketed by events
+    evsets = [make_events((jd, jd + 1)) for _ in range(K)]
     torch.cuda.synchronize()
     if args.flush:
+        step_ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+                   for _ in range(K)]
         for k in range(K):
             flush_buf.fill_(k & 0xFF)
+            step_ev[k][0].record(stream)
             check(lib.sangam_attn_forward_timed(*args_c, evsets[k][1]))
+            step_ev[k][1].record(stream)
         torch.cuda.synchronize()
-        step_ms = [evsets[k][0][0].elapsed_time(evsets[k][0][4]) for k in range(K)]
-        ms_per_step = float(np.mean(step_ms))
+        ms_per_step = float(np.mean([a.elapsed_time(b) for a, b in step_ev]))
     else:
         torch.cuda.synchronize()
         w0 = time.perf_counter()
@@ -211,22 +240,16 @@ def main():
             check(lib.sangam_attn_forward_timed(*args_c, evsets[k][1]))
         torch.cuda.synchronize()
         ms_per_step = (time.perf_counter() - w0) * 1e3 / K
+    dom_ms = float(np.mean([evsets[k][0][jd].elapsed_time(evsets[k][0][jd + 1]) for k in range(K)]))
     print(f"[bench] timed {K} steps: {ms_per_step:.4f} ms/step", file=sys.stderr, flush=True)
-
-    phase_ms = {}
-    for j, name in enumerate(PHASES):
-        phase_ms[name] = float(np.mean([evsets[k][0][j].elapsed_time(evsets[k][0][j + 1])
-                                        for k in range(K)]))
 
     F, B = wl.flops(), wl.hbm_bytes()
     sec = ms_per_step / 1e3
     tflops, gbs = F / sec / 1e12, B / sec / 1e9
     t_star = max(F / (PEAK_BF16_TFLOPS * 1e12), B / (PEAK_HBM_GBS * 1e9))
 
-    work = split_work(wl)
-    dom = max(("prefill_attn", "decode_attn"), key=lambda n: phase_ms[n] if work[n][0] > 0 else -1)
     f_d, b_d = work[dom]
-    t_d = phase_ms[dom] / 1e3
+    t_d = dom_ms / 1e3
     intensity = f_d / max(b_d, 1.0)
     if intensity >= PEAK_BF16_TFLOPS * 1e12 / (PEAK_HBM_GBS * 1e9):
         roof = {"bound": "mfma", "achieved": f_d / t_d / 1e12, "peak": PEAK_BF16_TFLOPS,
@@ -236,7 +259,7 @@ def main():
     roof["frac"] = roof["achieved"] / roof["peak"]
     roof["traffic"] = measured_traffic(wl.name, dom)
     roof["kernel"] = dom
-    roof["kernel_ms"] = phase_ms[dom]
+    roof["kernel_ms"] = dom_ms
     roof["algorithmic_flops"] = f_d
     roof["algorithmic_bytes"] = b_d
 

@@ -67,6 +67,39 @@ struct AttnArgs {
 
 __device__ __forceinline__ int uniform(int x) { return __builtin_amdgcn_readfirstlane(x); }
 
+// Asynchronous copy of 16 bytes per lane from global memory into LDS
+// (global_load_lds_dwordx4): lane l's bytes land at dst_wave + 16 l. Issued
+// through inline assembly so that the compiler does not track the LDS write:
+// it would otherwise wait for every copy in flight before any later LDS read,
+// including the copies that prefetch the next stage into another buffer,
+// which serialises the prefetch with the compute it should overlap. The
+// kernels order the copies themselves: s_waitcnt vmcnt and a barrier before a
+// staged buffer is read, a barrier before it is overwritten. M0 (the LDS
+// base) is saved and restored around the copy, with the wait state the
+// hardware needs between an M0 write and its use.
+__device__ __forceinline__ uint32_t lds_wave_base(LDS void* p) {
+    return __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)p);
+}
+__device__ __forceinline__ void lds_copy16(const void* src, LDS void* dst_wave) {
+    uint32_t saved;
+    asm volatile(
+        "s_mov_b32 %0, m0\n\ts_mov_b32 m0, %1\n\ts_nop 0\n\t"
+        "global_load_lds_dwordx4 %2, off\n\ts_nop 0\n\ts_mov_b32 m0, %0"
+        : "=&s"(saved)
+        : "s"(lds_wave_base(dst_wave)), "v"(src)
+        : "memory");
+}
+// the same from a wave-uniform base plus a per-lane 32-bit byte offset
+__device__ __forceinline__ void lds_copy16(const void* base, uint32_t off, LDS void* dst_wave) {
+    uint32_t saved;
+    asm volatile(
+        "s_mov_b32 %0, m0\n\ts_mov_b32 m0, %1\n\ts_nop 0\n\t"
+        "global_load_lds_dwordx4 %2, %3\n\ts_nop 0\n\ts_mov_b32 m0, %0"
+        : "=&s"(saved)
+        : "s"(lds_wave_base(dst_wave)), "v"(off), "s"(base)
+        : "memory");
+}
+
 // Swizzle of 16-byte chunks inside a staged key row. K rows are read one key
 // per lane (ds_read_b128), so consecutive keys rotate their chunks. V rows are
 // read four keys at a time by ds_read_b64_tr_b16, so groups of four keys
@@ -208,18 +241,14 @@ __global__ __launch_bounds__(64 * QW * KW, MINB) void attn_tiles_kernel(AttnArgs
         const bool tail = key0 + STEP > kv_end;
         if (all_fresh && !tail) {
             // uniform base + precomputed 32-bit offsets
-            // (the builtin's source must stay a pointer to the element type:
-            // a byte pointer there makes hipcc drop every kernel's host stub)
-            const uint8_t* kbase = reinterpret_cast<const uint8_t*>(kfresh + (size_t)key0 * row_stride);
-            const uint8_t* vbase = reinterpret_cast<const uint8_t*>(vfresh + (size_t)key0 * row_stride);
+            const uint16_t* kbase = kfresh + (size_t)key0 * row_stride;
+            const uint16_t* vbase = vfresh + (size_t)key0 * row_stride;
 #pragma unroll
             for (int j = 0; j < NJ; ++j) {
                 if ((NCH % NT) != 0 && j * NT + wave * 64 >= NCH) break;  // wave-uniform
                 const int dst = (j * NT + wave * 64) * 16;
-                __builtin_amdgcn_global_load_lds(reinterpret_cast<const uint16_t*>(kbase + foff_k[j]),
-                                                 (LDS void*)(kb + dst), 16, 0, 0);
-                __builtin_amdgcn_global_load_lds(reinterpret_cast<const uint16_t*>(vbase + foff_v[j]),
-                                                 (LDS void*)(vb + dst), 16, 0, 0);
+                lds_copy16(kbase, foff_k[j], (LDS void*)(kb + dst));
+                lds_copy16(vbase, foff_v[j], (LDS void*)(vb + dst));
             }
             return;
         }
@@ -243,8 +272,8 @@ __global__ __launch_bounds__(64 * QW * KW, MINB) void attn_tiles_kernel(AttnArgs
                 vsrc = vcache + off;
             }
             const int dst = (j * NT + wave * 64) * 16;
-            __builtin_amdgcn_global_load_lds(ksrc + ck, (LDS void*)(kb + dst), 16, 0, 0);
-            __builtin_amdgcn_global_load_lds(vsrc + cv, (LDS void*)(vb + dst), 16, 0, 0);
+            lds_copy16(ksrc + ck, (LDS void*)(kb + dst));
+            lds_copy16(vsrc + cv, (LDS void*)(vb + dst));
         }
     };
 
@@ -647,7 +676,7 @@ static sangam_status forward_impl(const void* plan_host, const void* plan_dev, c
     hipStream_t stream = static_cast<hipStream_t>(stream_ptr);
     const uint8_t* pd = static_cast<const uint8_t*>(plan_dev);
     auto mark = [&](int k) -> hipError_t {
-        return events ? hipEventRecord(static_cast<hipEvent_t>(events[k]), stream) : hipSuccess;
+        return events && events[k] ? hipEventRecord(static_cast<hipEvent_t>(events[k]), stream) : hipSuccess;
     };
     if (hipError_t e = mark(0); e != hipSuccess) return hip_fail(e, "event record");
     const ItemRec* items = reinterpret_cast<const ItemRec*>(pd + h->off_items);
@@ -748,11 +777,6 @@ extern "C" sangam_status sangam_attn_forward_timed(const void* plan_host, const 
         set_error("events must not be NULL");
         return SANGAM_ERR_INVALID_ARG;
     }
-    for (int k = 0; k < 5; ++k)
-        if (!events[k]) {
-            set_error("events must hold five HIP events");
-            return SANGAM_ERR_INVALID_ARG;
-        }
     return forward_impl(plan_host, plan_dev, q, k_new, v_new, k_cache, v_cache, page_ids_dev, out, lse,
                         workspace, workspace_bytes, stream, events);
 }
