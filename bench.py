@@ -32,8 +32,9 @@ PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
 PHASES = ("kv_write", "prefill_attn", "decode_attn", "merge")
 
 
-def split_work(wl):
-    """Algorithmic flops / bytes of each launch of the call."""
+def split_work(wl, fused_decodes=False):
+    """Algorithmic flops / bytes of each launch of the call. fused_decodes:
+    the plan runs the block decodes inside the prefill-shaped launch."""
     import numpy as np
     n = np.diff(wl.q_indptr).astype(np.float64)
     L = wl.kv_len.astype(np.float64)
@@ -44,9 +45,10 @@ def split_work(wl):
     attn_b = 2.0 * (2 * L * Hkv * D + 2 * n * Hq * D) + 4.0 * n * Hq
     attn_b += np.where(pre, 0.0, 4.0 * np.ceil(L / 16))
     write_b = 2.0 * (2 * n * Hkv * D) * 2  # read k_new/v_new, write them to pages
+    in_pre = np.ones_like(pre) if fused_decodes else pre
     return {
-        "prefill_attn": (float(flops[pre].sum()), float(attn_b[pre].sum())),
-        "decode_attn": (float(flops[~pre].sum()), float(attn_b[~pre].sum())),
+        "prefill_attn": (float(flops[in_pre].sum()), float(attn_b[in_pre].sum())),
+        "decode_attn": (float(flops[~in_pre].sum()), float(attn_b[~in_pre].sum())),
         "kv_write": (0.0, float(write_b.sum())),
     }
 
@@ -216,7 +218,7 @@ def main():
     for j, name in enumerate(PHASES):
         phase_ms[name] = float(np.mean([evsets[k][0][j].elapsed_time(evsets[k][0][j + 1])
                                         for k in range(n_phase)]))
-    work = split_work(wl)
+    work = split_work(wl, fused_decodes=int(p.info.num_fused_decode_tiles) > 0)
     dom = max(("prefill_attn", "decode_attn"), key=lambda n: phase_ms[n] if work[n][0] > 0 else -1)
     jd = PHASES.index(dom)
 

@@ -99,12 +99,16 @@ size_t sangam_plan_workspace_bytes(const void *plan_buf);
 typedef struct sangam_plan_info {
     int32_t num_items;
     int32_t num_decode_tiles;  /* work-groups of the decode-shaped launch (n_i <= 32) */
-    int32_t num_prefill_tiles; /* work-groups of the prefill-shaped launch (n_i > 32) */
+    int32_t num_prefill_tiles; /* work-groups of the prefill-shaped launch (n_i > 32, and
+                                  the fused block decodes below) */
     int32_t num_split_items;   /* items whose context is split (merged afterwards) */
     int32_t max_splits;        /* largest split count of an item */
     int32_t decode_q_waves;    /* waves per decode work-group that hold query rows */
     int32_t decode_kv_waves;   /* waves per decode work-group that split the context */
-    int32_t reserved;
+    int32_t num_fused_decode_tiles; /* prefill-shaped work-groups that hold block decodes:
+                                       in a batch with prefills, a GQA group of >= 4 query
+                                       heads per KV head puts its block decodes there (one
+                                       query head per wave), unsplit up to 8192 keys */
     int64_t total_q_rows;      /* sum n_i */
     int64_t workspace_bytes;
     int64_t plan_bytes;

@@ -68,7 +68,7 @@ class PlanInfo(ctypes.Structure):
         ("max_splits", ctypes.c_int32),
         ("decode_q_waves", ctypes.c_int32),
         ("decode_kv_waves", ctypes.c_int32),
-        ("reserved", ctypes.c_int32),
+        ("num_fused_decode_tiles", ctypes.c_int32),
         ("total_q_rows", ctypes.c_int64),
         ("workspace_bytes", ctypes.c_int64),
         ("plan_bytes", ctypes.c_int64),

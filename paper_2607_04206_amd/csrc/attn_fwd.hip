@@ -185,8 +185,15 @@ __global__ __launch_bounds__(64 * QW * KW, MINB) void attn_tiles_kernel(AttnArgs
 
     const TileRec t = a.tiles[blockIdx.x];
     const ItemRec it = a.items[t.item];
-    const int head = HEADS_ACROSS ? t.q_head0 + qs : t.q_head0;
-    const int row_base = HEADS_ACROSS ? t.row0 : t.row0 + 32 * QB * qs;
+    // heads across the waves: a decode-shaped work-group, or a block decode
+    // cut into a prefill-shaped one (whose last tile of a GQA group may hold
+    // fewer heads than waves: the extra waves compute with the tile's first
+    // head and store nothing)
+    const bool across = HEADS_ACROSS || (t.flags & kTileHeadsAcross);
+    const int head_want = across ? t.q_head0 + qs : t.q_head0;
+    const bool head_ok = head_want < (t.kv_head + 1) * (a.hq / a.hkv);
+    const int head = head_ok ? head_want : t.q_head0;
+    const int row_base = across ? t.row0 : t.row0 + 32 * QB * qs;
     const int kv_begin = t.kv_begin, kv_end = t.kv_end;
     const int nstages = (kv_end - kv_begin + STEP - 1) / STEP;
     // a whole prefill brings every position fresh: no page lookups
@@ -493,7 +500,7 @@ __global__ __launch_bounds__(64 * QW * KW, MINB) void attn_tiles_kernel(AttnArgs
         const float l_tot = half_sum(l_run[qb]);
         const float inv = 1.0f / l_tot;
         const float lse_val = m_used[qb] * 0.69314718055994530942f + logf(l_tot);
-        if (row >= it.n) continue;
+        if (row >= it.n || !head_ok) continue;
         if (it.num_splits > 1) {
             const size_t prow = (size_t)(t.split * it.n + row) * a.hq + head;
             float* po = a.ws + it.ws_o + prow * D;

@@ -14,6 +14,12 @@
 //   prefill-shaped (n_i > 32, a whole prefill): one work-group per (item,
 //                  query head, 128-row block); four waves of 32 rows share
 //                  each staged K/V tile.
+// In a batch that holds prefills, block decodes whose GQA group has at least
+// four query heads are cut into prefill-shaped work-groups instead (one query
+// head per wave, kTileHeadsAcross): they join the prefill launch, where the
+// longest-first order puts them last, so they fill the tail of the prefill
+// work rather than running after it, and they are split only where the
+// context range limit requires (no split, no merge for typical contexts).
 #include <algorithm>
 #include <cstring>
 #include <numeric>
@@ -144,15 +150,22 @@ extern "C" sangam_status sangam_attn_plan(const sangam_attn_desc* d, void* plan_
     // ---- splits: decode-shaped contexts longer than kForcedSplitLen are always
     // split; others are cut so that the decode launch has about four
     // work-groups per CU. Prefill-shaped items already give one work-group per
-    // 128 rows and head, so they are split only on request.
+    // 128 rows and head, and block decodes fused into the prefill launch run
+    // beside them, so both are split only on request (or where the context
+    // range limit of cached rows requires it).
     const int qw = decode_q_waves(G);
     const int kw = decode_kv_waves(qw);
     const int heads_per_tile = qw;
     const int tiles_per_kv_head = G / heads_per_tile;
+    bool has_prefill = false;
+    for (int i = 0; i < n_items && !has_prefill; ++i)
+        has_prefill = int64_t(d->q_indptr[i + 1]) - d->q_indptr[i] > kWaveRows;
+    const bool fuse = has_prefill && G >= kPrefillQWaves;
+    const int fused_tiles_per_kv_head = int(ceil_div(G, kPrefillQWaves));
     int64_t decode_keys = 0;
     for (int i = 0; i < n_items; ++i) {
         const int64_t n = int64_t(d->q_indptr[i + 1]) - d->q_indptr[i];
-        if (n <= kWaveRows) decode_keys += int64_t(hkv) * tiles_per_kv_head * d->kv_len[i];
+        if (n <= kWaveRows && !fuse) decode_keys += int64_t(hkv) * tiles_per_kv_head * d->kv_len[i];
     }
     int64_t chunk = ceil_div(decode_keys, 4 * int64_t(num_cus));
     chunk = std::min<int64_t>(std::max<int64_t>(round_up(std::max<int64_t>(chunk, 1), kKeyAlign), min_chunk(qw)),
@@ -171,8 +184,10 @@ extern "C" sangam_status sangam_attn_plan(const sangam_attn_desc* d, void* plan_
         int64_t S;
         if (d->force_kv_splits > 0) {
             S = std::min<int64_t>(d->force_kv_splits, ceil_div(it.L, kKeyAlign));
-        } else if (it.n <= kWaveRows) {
+        } else if (it.n <= kWaveRows && !fuse) {
             S = std::max<int64_t>(ceil_div(it.L, kForcedSplitLen), ceil_div(it.L, chunk));
+        } else if (it.n <= kWaveRows) {
+            S = ceil_div(it.L, kForcedSplitLen);
         } else {
             S = 1;
         }
@@ -203,12 +218,21 @@ extern "C" sangam_status sangam_attn_plan(const sangam_attn_desc* d, void* plan_
     // ---- tiles
     std::vector<TileRec> dec, pre;
     std::vector<int64_t> dec_cost, pre_cost;
+    int64_t n_fused = 0;  // (item, chunk) pairs cut into prefill-shaped tiles
     for (int i = 0; i < n_items; ++i) {
         const ItemRec& it = items[i];
         for (int s = 0; s < it.num_splits; ++s) {
             const int32_t kb = s * it.split_len;
             const int32_t ke = std::min<int32_t>(it.L, kb + it.split_len);
-            if (it.n <= kWaveRows) {
+            if (it.n <= kWaveRows && fuse) {
+                for (int g = 0; g < hkv; ++g)
+                    for (int t = 0; t < fused_tiles_per_kv_head; ++t) {
+                        TileRec tr{i, g, g * G + t * kPrefillQWaves, 0, kb, ke, s, kTileHeadsAcross};
+                        pre.push_back(tr);
+                        pre_cost.push_back(int64_t(ke - kb) * kPrefillQWaves);
+                    }
+                ++n_fused;
+            } else if (it.n <= kWaveRows) {
                 for (int g = 0; g < hkv; ++g)
                     for (int t = 0; t < tiles_per_kv_head; ++t) {
                         TileRec tr{i, g, g * G + t * heads_per_tile, 0, kb, ke, s, 0};
@@ -290,6 +314,7 @@ extern "C" sangam_status sangam_attn_plan(const sangam_attn_desc* d, void* plan_
     h.num_split_items = n_split_items;
     h.max_splits = max_splits;
     h.prefill_rows = kPrefillRows;
+    h.n_fused_decode_tiles = int32_t(n_fused * hkv * fused_tiles_per_kv_head);
     h.workspace_bytes = ws_floats * int64_t(sizeof(float));
     h.off_items = off_items;
     h.off_decode_tiles = off_dec;
@@ -320,7 +345,7 @@ extern "C" sangam_status sangam_plan_get_info(const void* plan_buf, sangam_plan_
     info->max_splits = h->max_splits;
     info->decode_q_waves = h->decode_qw;
     info->decode_kv_waves = h->decode_kw;
-    info->reserved = 0;
+    info->num_fused_decode_tiles = h->n_fused_decode_tiles;
     info->total_q_rows = h->total_q;
     info->workspace_bytes = h->workspace_bytes;
     info->plan_bytes = int64_t(h->total_bytes);

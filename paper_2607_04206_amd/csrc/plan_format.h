@@ -9,7 +9,7 @@
 namespace sangam {
 
 constexpr uint32_t kPlanMagic = 0x50414753u;  // "SGAP"
-constexpr uint32_t kPlanVersion = 1;
+constexpr uint32_t kPlanVersion = 2;
 
 constexpr int kWaveRows = 32;       // query rows held by one wave (one decode block)
 constexpr int kPrefillQWaves = 4;   // waves of a prefill-shaped work-group
@@ -35,6 +35,11 @@ struct ItemRec {
     int64_t ws_lse;      // float offset of partial LSE [num_splits][n][Hq]
 };
 
+// TileRec.flags: the waves of a prefill-shaped work-group hold consecutive
+// query heads (q_head0 + wave, those inside the tile's GQA group) of one
+// block decode instead of consecutive 32-row blocks of one head.
+constexpr int32_t kTileHeadsAcross = 1;
+
 // One work-group of an attention launch.
 struct TileRec {
     int32_t item;
@@ -44,7 +49,7 @@ struct TileRec {
     int32_t kv_begin;  // context range [kv_begin, kv_end)
     int32_t kv_end;
     int32_t split;     // chunk index of the context
-    int32_t reserved;
+    int32_t flags;     // kTileHeadsAcross or 0
 };
 
 // One (item, row) whose split partial results the merge kernel combines.
@@ -77,13 +82,18 @@ struct PlanHeader {
     int32_t decode_kw;
     int32_t decode_nb;   // 32-key blocks per wave per stage
     // prefill-shaped launch: items with n > kWaveRows; kPrefillQWaves waves
-    // of 32 rows of one query head
+    // of 32 rows of one query head. In a batch that holds prefills, block
+    // decodes whose GQA group spans at least kPrefillQWaves query heads run
+    // in this launch too (kTileHeadsAcross tiles, n_fused_decode_tiles of
+    // n_prefill_tiles), filling its tail instead of a launch of their own.
     int32_t n_prefill_tiles;
     int32_t prefill_nb;
     int32_t n_merge_rows;
     int32_t num_split_items;
     int32_t max_splits;
     int32_t prefill_rows;  // query rows per prefill-shaped tile
+    int32_t n_fused_decode_tiles;
+    int32_t reserved;
     int64_t workspace_bytes;
 
     uint64_t off_items;
@@ -95,6 +105,6 @@ struct PlanHeader {
 static_assert(sizeof(ItemRec) == 48, "ItemRec layout is part of the blob format");
 static_assert(sizeof(TileRec) == 32, "TileRec layout is part of the blob format");
 static_assert(sizeof(MergeRow) == 8, "MergeRow layout is part of the blob format");
-static_assert(sizeof(PlanHeader) == 152, "PlanHeader layout is part of the blob format");
+static_assert(sizeof(PlanHeader) == 160, "PlanHeader layout is part of the blob format");
 
 }  // namespace sangam

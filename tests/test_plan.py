@@ -18,14 +18,15 @@ HEADER = np.dtype([
     ("n_decode_tiles", "<i4"), ("decode_qw", "<i4"), ("decode_kw", "<i4"), ("decode_nb", "<i4"),
     ("n_prefill_tiles", "<i4"), ("prefill_nb", "<i4"), ("n_merge_rows", "<i4"),
     ("num_split_items", "<i4"), ("max_splits", "<i4"), ("prefill_rows", "<i4"),
-    ("workspace_bytes", "<i8"),
+    ("n_fused_decode_tiles", "<i4"), ("reserved", "<i4"), ("workspace_bytes", "<i8"),
     ("off_items", "<u8"), ("off_decode_tiles", "<u8"), ("off_prefill_tiles", "<u8"), ("off_merge", "<u8"),
 ])
 ITEM = np.dtype([("q_start", "<i4"), ("n", "<i4"), ("o", "<i4"), ("L", "<i4"), ("page_start", "<i4"),
                  ("num_splits", "<i4"), ("split_len", "<i4"), ("merge_base", "<i4"),
                  ("ws_o", "<i8"), ("ws_lse", "<i8")])
 TILE = np.dtype([("item", "<i4"), ("kv_head", "<i4"), ("q_head0", "<i4"), ("row0", "<i4"),
-                 ("kv_begin", "<i4"), ("kv_end", "<i4"), ("split", "<i4"), ("reserved", "<i4")])
+                 ("kv_begin", "<i4"), ("kv_end", "<i4"), ("split", "<i4"), ("flags", "<i4")])
+HEADS_ACROSS = 1
 MERGE = np.dtype([("item", "<i4"), ("row", "<i4")])
 
 
@@ -51,9 +52,9 @@ def test_header_size_matches():
     # plan_format.h static_asserts the same sizes on the C side
     p = plan_of(workloads.tiny_mixed(0))
     h, *_ = parse(p)
-    assert h["magic"] == 0x50414753 and h["version"] == 1
+    assert h["magic"] == 0x50414753 and h["version"] == 2
     assert h["total_bytes"] == p.host.nbytes
-    assert HEADER.itemsize == 152 and ITEM.itemsize == 48 and TILE.itemsize == 32
+    assert HEADER.itemsize == 160 and ITEM.itemsize == 48 and TILE.itemsize == 32
 
 
 def coverage(wl, p):
@@ -71,11 +72,19 @@ def coverage(wl, p):
         for hd in range(int(t["q_head0"]), int(t["q_head0"]) + qw):
             assert hd // G == t["kv_head"]
             cover[i][hd, :, t["kv_begin"]:t["kv_end"]] += 1
+    waves = rows // 32
     for t in pre:
         i = int(t["item"])
-        assert wl.n(i) > 32
         hd = int(t["q_head0"])
         assert hd // G == t["kv_head"]
+        if t["flags"] & HEADS_ACROSS:
+            # a block decode in the prefill launch: one head per wave, only
+            # those inside the tile's GQA group
+            assert wl.n(i) <= 32 and t["row0"] == 0
+            for h2 in range(hd, min(hd + waves, (int(t["kv_head"]) + 1) * G)):
+                cover[i][h2, :, t["kv_begin"]:t["kv_end"]] += 1
+            continue
+        assert wl.n(i) > 32 and t["flags"] == 0
         r0 = int(t["row0"])
         cover[i][hd, r0:r0 + rows, t["kv_begin"]:t["kv_end"]] += 1
     return cover
@@ -90,6 +99,9 @@ def coverage(wl, p):
     lambda: workloads.ragged_small(0, hq=11, hkv=1, d=128),
     lambda: workloads.llada_decode(1),
     lambda: workloads.dream_mixed(2),
+    lambda: workloads.make_workload("g7", 3, hq=28, hkv=4, d=128, decodes=[(0, 9000), (64, 300)],
+                                    prefills=[200]),
+    lambda: workloads.make_workload("g2", 4, hq=8, hkv=4, d=64, decodes=[(32, 700)], prefills=[100]),
 ])
 @pytest.mark.parametrize("force", [0, 1, 3, 8])
 def test_every_row_head_key_covered_once(mk, force):
@@ -97,6 +109,38 @@ def test_every_row_head_key_covered_once(mk, force):
     p = plan_of(wl, force_kv_splits=force)
     for i, c in coverage(wl, p).items():
         assert c.min() == 1 and c.max() == 1, f"item {i}"
+
+
+def test_block_decodes_fuse_into_prefill_launch():
+    # GQA groups of >= 4 heads: a mixed batch runs its block decodes as
+    # heads-across tiles of the prefill launch, unsplit below 8192 keys
+    wl = workloads.dream_mixed(0)
+    p = plan_of(wl)
+    h, items, dec, pre, mer = parse(p)
+    n_dec = sum(1 for i in range(wl.num_items) if wl.n(i) <= 32)
+    G = wl.num_q_heads // wl.num_kv_heads
+    assert len(dec) == 0 and len(mer) == 0 and p.workspace_bytes == 0
+    fused = pre[(pre["flags"] & HEADS_ACROSS) != 0]
+    assert len(fused) == h["n_fused_decode_tiles"] == p.info.num_fused_decode_tiles
+    assert len(fused) == n_dec * wl.num_kv_heads * -(-G // 4)
+    # longest first: every prefill tile is at least as long as any fused one
+    cost = (pre["kv_end"] - pre["kv_begin"]).astype(np.int64) * 4
+    assert np.all(np.diff(cost) <= 0)
+    # a decode context over 8192 keys is still split (and merged)
+    wl2 = workloads.make_workload("g7", 3, hq=28, hkv=4, d=128, decodes=[(0, 9000), (64, 300)],
+                                  prefills=[200])
+    p2 = plan_of(wl2)
+    _, items2, dec2, pre2, mer2 = parse(p2)
+    assert len(dec2) == 0
+    assert items2[0]["num_splits"] == 2 and items2[1]["num_splits"] == 1
+    assert len(mer2) == wl2.n(0)
+    # pure decode batches and small groups keep the decode launch
+    for wl3 in (workloads.llada_decode(0),
+                workloads.make_workload("g2", 4, hq=8, hkv=4, d=64, decodes=[(32, 700)], prefills=[100])):
+        p3 = plan_of(wl3)
+        _, _, dec3, pre3, _ = parse(p3)
+        assert len(dec3) > 0 and not np.any(pre3["flags"] & HEADS_ACROSS)
+        assert p3.info.num_fused_decode_tiles == 0
 
 
 def test_splits_and_merge_rows():
@@ -142,14 +186,18 @@ def test_forced_split_count():
 
 
 def test_longest_first():
-    p = plan_of(workloads.dream_mixed(0))
-    _, items, dec, pre, _ = parse(p)
-    dc = dec["kv_end"] - dec["kv_begin"]
-    assert np.all(np.diff(dc) <= 0)
-    h = parse(p)[0]
-    rows = np.minimum(int(h["prefill_rows"]), items["n"][pre["item"]] - pre["row0"])
-    pc = (pre["kv_end"] - pre["kv_begin"]) * ((rows + 31) // 32)
-    assert np.all(np.diff(pc) <= 0)
+    # cost = keys x waves holding rows (a fused block decode keeps all four busy)
+    for wl in (workloads.dream_mixed(0), workloads.llada_decode(0),
+               workloads.make_workload("m", 5, hq=8, hkv=8, d=128, decodes=[(0, 3000), (32, 900)],
+                                       prefills=[300, 1000])):
+        p = plan_of(wl)
+        h, items, dec, pre, _ = parse(p)
+        dc = dec["kv_end"] - dec["kv_begin"]
+        assert np.all(np.diff(dc) <= 0)
+        waves = int(h["prefill_rows"]) // 32
+        rows = np.minimum(int(h["prefill_rows"]), items["n"][pre["item"]] - pre["row0"])
+        pc = (pre["kv_end"] - pre["kv_begin"]) * np.where(pre["flags"] & HEADS_ACROSS, waves, (rows + 31) // 32)
+        assert np.all(np.diff(pc) <= 0)
 
 
 def test_deterministic_bytes():
