@@ -1,13 +1,14 @@
 #!/usr/bin/env python3
 """Benchmark of the mixed block-decode / prefill attention call on one MI355X.
 
-A step is one whole call: KV write-back, the prefill-shaped and the
-decode-shaped attention launches and the split merge, over one batch whose
-inputs are already resident in HBM. Prints one JSON line (rank 0).
+A step is one whole call: the prefill-shaped and the decode-shaped attention
+launches (which also write the fresh K/V rows back into their pages) and the
+split merge, over one batch whose inputs are already resident in HBM. Prints
+one JSON line (rank 0).
 
     python bench.py [--steps K] [--warmup W] [--workload NAME] [--seed S]
 
-Timing: a short untimed pass records events between all four phases (the
+Timing: a short untimed pass records events between all three launches (the
 phase breakdown); the timed region then runs K whole steps with events only
 around the dominant attention launch, whose average duration gives the
 roofline figure. ms_per_step is host wall time over the K steps, bracketed by
@@ -29,27 +30,28 @@ sys.path.insert(0, ROOT)
 METRIC = "attention TFLOP/s + KV HBM GB/s (frac. of roofline), mixed decode/prefill batch"
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
-PHASES = ("kv_write", "prefill_attn", "decode_attn", "merge")
+PHASES = ("prefill_attn", "decode_attn", "merge")
 
 
 def split_work(wl, fused_decodes=False):
-    """Algorithmic flops / bytes of each launch of the call. fused_decodes:
-    the plan runs the block decodes inside the prefill-shaped launch."""
+    """Algorithmic flops / bytes of each attention launch of the call.
+    fused_decodes: the plan runs the block decodes inside the prefill-shaped
+    launch. Each launch also writes back the fresh rows of its items."""
     import numpy as np
     n = np.diff(wl.q_indptr).astype(np.float64)
     L = wl.kv_len.astype(np.float64)
     D, Hq, Hkv = wl.head_dim, wl.num_q_heads, wl.num_kv_heads
     pre = n > 32
     flops = 4.0 * n * L * D * Hq
-    # attention launch: K/V read once, Q read, O write, LSE write, page ids (decode)
+    # K/V read once, Q read, O write, LSE write, page ids (decode), and the
+    # fresh rows written into their pages
     attn_b = 2.0 * (2 * L * Hkv * D + 2 * n * Hq * D) + 4.0 * n * Hq
     attn_b += np.where(pre, 0.0, 4.0 * np.ceil(L / 16))
-    write_b = 2.0 * (2 * n * Hkv * D) * 2  # read k_new/v_new, write them to pages
+    attn_b += 2.0 * (2 * n * Hkv * D)
     in_pre = np.ones_like(pre) if fused_decodes else pre
     return {
         "prefill_attn": (float(flops[in_pre].sum()), float(attn_b[in_pre].sum())),
         "decode_attn": (float(flops[~in_pre].sum()), float(attn_b[~in_pre].sum())),
-        "kv_write": (0.0, float(write_b.sum())),
     }
 
 
@@ -181,13 +183,13 @@ def main():
               t["page_ids"].data_ptr(), out.data_ptr(), lse.data_ptr(), ws.data_ptr(), ws.numel(),
               stream.cuda_stream]
 
-    def make_events(which=range(5)):
-        """Five event slots; slots outside `which` stay NULL (nothing recorded)."""
-        evs = [torch.cuda.Event(enable_timing=True) if j in which else None for j in range(5)]
+    def make_events(which=range(4)):
+        """Four event slots; slots outside `which` stay NULL (nothing recorded)."""
+        evs = [torch.cuda.Event(enable_timing=True) if j in which else None for j in range(4)]
         for e in evs:
             if e is not None:
                 e.record(stream)  # creates the HIP event
-        arr = (ctypes.c_void_p * 5)(*[e.cuda_event if e is not None else None for e in evs])
+        arr = (ctypes.c_void_p * 4)(*[e.cuda_event if e is not None else None for e in evs])
         return evs, arr
 
     flush_buf = torch.empty((512 << 20,), dtype=torch.uint8, device=dev) if args.flush else None
@@ -204,7 +206,7 @@ def main():
     torch.cuda.synchronize()
     print(f"[bench] warmup done ({args.warmup} steps)", file=sys.stderr, flush=True)
 
-    # phase breakdown, outside the timed region: events between all four phases
+    # phase breakdown, outside the timed region: events between all three launches
     K = args.steps
     n_phase = max(3, min(K, 10))
     evsets = [make_events() for _ in range(n_phase)]

@@ -10,9 +10,10 @@
 // Sec. 6.1).
 //
 // Kernels:
-//   kv_write_kernel   scatters k_new / v_new rows into their cache pages.
 //   attn_tiles_kernel one work-group per plan tile: a context range of one
-//                     item and KV head against up to 8 x 32 query rows.
+//                     item and KV head against up to 8 x 32 query rows; one
+//                     tile per item, KV head and row block also copies the
+//                     fresh K/V rows into their cache pages.
 //                     Per wave: S^T = K Q^T with v_mfma_f32_32x32x16_bf16
 //                     (each lane holds the scores of one query, so row max /
 //                     row sum need one cross-half exchange), online softmax
@@ -55,8 +56,8 @@ struct AttnArgs {
     const uint16_t* q;
     const uint16_t* k_new;
     const uint16_t* v_new;
-    const uint16_t* k_cache;
-    const uint16_t* v_cache;
+    uint16_t* k_cache;  // read (cached rows) and written (the fresh rows' pages)
+    uint16_t* v_cache;
     uint16_t* out;
     float* lse;
     float* ws;
@@ -167,6 +168,7 @@ __global__ __launch_bounds__(64 * QW * KW, MINB) void attn_tiles_kernel(AttnArgs
     static_assert(KW == 1 || (QW * (KW - 1) * MERGE_REGS * 64 * 4) <= 2 * NSTAGE * TILE,
                   "cross-wave merge must fit in the stage buffers");
     static_assert(NSTAGE >= 2 && NSTAGE <= 4, "2 to 4 stage buffers");
+    static_assert(HEADS_ACROSS || 32 * QB * QW <= 240, "a tile writes back at most 16 pages");
     // with more than two buffers the wait counts loads, so every wave must
     // issue the same number per stage
     static_assert(NSTAGE == 2 || NCH % NT == 0, "deeper pipelines need whole staging rounds");
@@ -174,6 +176,7 @@ __global__ __launch_bounds__(64 * QW * KW, MINB) void attn_tiles_kernel(AttnArgs
 
     __shared__ __attribute__((aligned(1024))) uint8_t smem[2 * NSTAGE * TILE];
     __shared__ int32_t pages[MAX_PAGES];
+    __shared__ int32_t wpages[16];  // pages of the fresh rows this tile writes back
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -281,6 +284,40 @@ __global__ __launch_bounds__(64 * QW * KW, MINB) void attn_tiles_kernel(AttnArgs
             const int dst = (j * NT + wave * 64) * 16;
             lds_copy16(ksrc + ck, (LDS void*)(kb + dst));
             lds_copy16(vsrc + cv, (LDS void*)(vb + dst));
+        }
+    };
+
+    // ---- write-back of the fresh K/V rows into their cache pages. Per item
+    // and KV head, the tiles of the group's first query head copy the fresh
+    // rows they stage (a prefill tile its own row block, a block decode its
+    // rows) from LDS, right after the stage lands: no second read of k_new /
+    // v_new. Every fresh position lies in exactly one such tile's row block
+    // and context range. No tile reads these cache rows (fresh positions come
+    // from k_new / v_new, and the planner rejects pages shared between items),
+    // so the copy needs no ordering with the attention. The pages of the
+    // written range (at most 9) are staged in LDS once, right after the first
+    // stage is issued (their wait overlaps that stage's), so the copy loop
+    // issues no global load whose wait would also drain the prefetch.
+    const int group = a.hq / a.hkv;
+    const bool wb_head = across ? t.q_head0 == t.kv_head * group : t.q_head0 % group == 0;
+    const int wb_lo = max(kv_begin, it.o + (across ? 0 : t.row0));
+    const int wb_hi = min(kv_end, it.o + (across ? it.n : min(it.n, t.row0 + 32 * QB * QW)));
+    const bool writer = wb_head && wb_lo < wb_hi;
+    const int wpg0 = wb_lo >> 4;
+    auto write_back = [&](int st) {
+        const int key0 = kv_begin + st * STEP;
+        const int lo = max(wb_lo, key0), hi = min(wb_hi, key0 + STEP);
+        if (lo >= hi) return;
+        const uint8_t* kb = smem + (st % NSTAGE) * 2 * TILE;
+        const uint8_t* vb = kb + TILE;
+        for (int cidx = tid; cidx < (hi - lo) * NC; cidx += NT) {
+            const int p = lo + cidx / NC, pos = cidx % NC;
+            const int r = p - key0;
+            const u32x4 kv = *(const LDS u32x4*)(kb + r * ROWB + ((pos ^ swz_k<D>(r)) << 4));
+            const u32x4 vv = *(const LDS u32x4*)(vb + r * ROWB + ((pos ^ swz_v<D>(r)) << 4));
+            const size_t dst = (((size_t)wpages[(p >> 4) - wpg0] * a.hkv + t.kv_head) * 16 + (p & 15)) * D + pos * 8;
+            *(u32x4*)(a.k_cache + dst) = kv;
+            *(u32x4*)(a.v_cache + dst) = vv;
         }
     };
 
@@ -435,11 +472,13 @@ __global__ __launch_bounds__(64 * QW * KW, MINB) void attn_tiles_kernel(AttnArgs
             asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     };
     for (int k = 0; k < NSTAGE - 1 && k < nstages; ++k) issue_stage(k, k);
+    if (writer && tid < ((wb_hi + 15) >> 4) - wpg0) wpages[tid] = a.page_ids[it.page_start + wpg0 + tid];
     int st = 0;
     for (; st < full_stages; ++st) {
         wait_stage(st);
         __syncthreads();
         if (st + NSTAGE - 1 < nstages) issue_stage(st + NSTAGE - 1, (st + NSTAGE - 1) % NSTAGE);
+        if (writer) write_back(st);
         f32x16 sc[QB][NB];
         qk(st, sc);
         softmax_pv(st, sc, false);
@@ -447,6 +486,7 @@ __global__ __launch_bounds__(64 * QW * KW, MINB) void attn_tiles_kernel(AttnArgs
     if (st < nstages) {  // the last, partial stage
         asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
         __syncthreads();
+        if (writer) write_back(st);
         f32x16 sc[QB][NB];
         qk(st, sc);
         softmax_pv(st, sc, true);
@@ -529,43 +569,6 @@ __global__ __launch_bounds__(64 * QW * KW, MINB) void attn_tiles_kernel(AttnArgs
             if (hh == 0 && a.lse) a.lse[(size_t)(it.q_start + row) * a.hq + head] = lse_val;
         }
     }
-}
-
-// ---------------------------------------------------------------- KV write
-struct WriteArgs {
-    const ItemRec* items;
-    const int32_t* page_ids;
-    const uint16_t* k_new;
-    const uint16_t* v_new;
-    uint16_t* k_cache;
-    uint16_t* v_cache;
-    int32_t n_items;
-    int32_t hkv;
-    int32_t d;
-    int64_t total_chunks;  // total_q * hkv * d / 8
-};
-
-__global__ __launch_bounds__(256) void kv_write_kernel(WriteArgs a) {
-    const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
-    if (idx >= a.total_chunks) return;
-    const int cpr = a.d / 8;
-    const int64_t row = idx / (a.hkv * cpr);
-    const int rem = int(idx - row * a.hkv * cpr);
-    const int g = rem / cpr;
-    const int c = rem - g * cpr;
-    int lo = 0, hi = a.n_items - 1;
-    while (lo < hi) {
-        const int mid = (lo + hi + 1) >> 1;
-        if (a.items[mid].q_start <= row) lo = mid;
-        else hi = mid - 1;
-    }
-    const ItemRec& it = a.items[lo];
-    const int p = it.o + int(row - it.q_start);
-    const int page = a.page_ids[it.page_start + (p >> 4)];
-    const size_t dst = (((size_t)page * a.hkv + g) * 16 + (p & 15)) * a.d + c * 8;
-    const size_t src = ((size_t)row * a.hkv + g) * a.d + c * 8;
-    *(u32x4*)(a.k_cache + dst) = *(const u32x4*)(a.k_new + src);
-    *(u32x4*)(a.v_cache + dst) = *(const u32x4*)(a.v_new + src);
 }
 
 // --------------------------------------------------------------- split merge
@@ -685,27 +688,8 @@ static sangam_status forward_impl(const void* plan_host, const void* plan_dev, c
     auto mark = [&](int k) -> hipError_t {
         return events && events[k] ? hipEventRecord(static_cast<hipEvent_t>(events[k]), stream) : hipSuccess;
     };
-    if (hipError_t e = mark(0); e != hipSuccess) return hip_fail(e, "event record");
     const ItemRec* items = reinterpret_cast<const ItemRec*>(pd + h->off_items);
-
-    // 1. write the fresh rows into their pages
-    if (h->total_q > 0) {
-        WriteArgs w{items,
-                    page_ids_dev,
-                    static_cast<const uint16_t*>(k_new),
-                    static_cast<const uint16_t*>(v_new),
-                    static_cast<uint16_t*>(k_cache),
-                    static_cast<uint16_t*>(v_cache),
-                    h->num_items,
-                    h->hkv,
-                    h->d,
-                    h->total_q * h->hkv * (h->d / 8)};
-        const int64_t blocks = (w.total_chunks + 255) / 256;
-        kv_write_kernel<<<dim3(unsigned(blocks)), dim3(256), 0, stream>>>(w);
-        hipError_t e = hipGetLastError();
-        if (e != hipSuccess) return hip_fail(e, "kv write launch");
-    }
-    if (hipError_t e = mark(1); e != hipSuccess) return hip_fail(e, "event record");
+    if (hipError_t e = mark(0); e != hipSuccess) return hip_fail(e, "event record");
 
     AttnArgs args{nullptr,
                   items,
@@ -713,8 +697,8 @@ static sangam_status forward_impl(const void* plan_host, const void* plan_dev, c
                   static_cast<const uint16_t*>(q),
                   static_cast<const uint16_t*>(k_new),
                   static_cast<const uint16_t*>(v_new),
-                  static_cast<const uint16_t*>(k_cache),
-                  static_cast<const uint16_t*>(v_cache),
+                  static_cast<uint16_t*>(k_cache),
+                  static_cast<uint16_t*>(v_cache),
                   static_cast<uint16_t*>(out),
                   lse,
                   static_cast<float*>(workspace),
@@ -722,7 +706,8 @@ static sangam_status forward_impl(const void* plan_host, const void* plan_dev, c
                   h->hkv,
                   h->scale_log2};
 
-    // 2. prefill-shaped tiles (compute-bound) first, then decode-shaped tiles
+    // 1. attention: prefill-shaped tiles (compute-bound) first, then
+    // decode-shaped tiles; both also write the fresh rows into their pages
     if (h->n_prefill_tiles > 0) {
         args.tiles = reinterpret_cast<const TileRec*>(pd + h->off_prefill_tiles);
         hipError_t e = h->d == 128
@@ -730,7 +715,7 @@ static sangam_status forward_impl(const void* plan_host, const void* plan_dev, c
                            : launch_tiles<64, kPrefillQWaves, 1, kPrefillQBlocks, 2, false>(args, h->n_prefill_tiles, stream);
         if (e != hipSuccess) return hip_fail(e, "prefill attention launch");
     }
-    if (hipError_t e = mark(2); e != hipSuccess) return hip_fail(e, "event record");
+    if (hipError_t e = mark(1); e != hipSuccess) return hip_fail(e, "event record");
     if (h->n_decode_tiles > 0) {
         args.tiles = reinterpret_cast<const TileRec*>(pd + h->off_decode_tiles);
         bool ok = false;
@@ -744,9 +729,9 @@ static sangam_status forward_impl(const void* plan_host, const void* plan_dev, c
         }
         if (e != hipSuccess) return hip_fail(e, "decode attention launch");
     }
-    if (hipError_t e = mark(3); e != hipSuccess) return hip_fail(e, "event record");
+    if (hipError_t e = mark(2); e != hipSuccess) return hip_fail(e, "event record");
 
-    // 3. merge split contexts
+    // 2. merge split contexts
     if (h->n_merge_rows > 0) {
         MergeArgs m{reinterpret_cast<const MergeRow*>(pd + h->off_merge),
                     items,
@@ -759,7 +744,7 @@ static sangam_status forward_impl(const void* plan_host, const void* plan_dev, c
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return hip_fail(e, "merge launch");
     }
-    if (hipError_t e = mark(4); e != hipSuccess) return hip_fail(e, "event record");
+    if (hipError_t e = mark(3); e != hipSuccess) return hip_fail(e, "event record");
     return SANGAM_OK;
 }
 
