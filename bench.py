@@ -8,11 +8,11 @@ one JSON line (rank 0).
 
     python bench.py [--steps K] [--warmup W] [--workload NAME] [--seed S]
 
-Timing: a short untimed pass records events between all three launches (the
-phase breakdown); the timed region then runs K whole steps with events only
-around the dominant attention launch, whose average duration gives the
-roofline figure. ms_per_step is host wall time over the K steps, bracketed by
-device synchronisation.
+Timing: a short untimed pass times each of the three launches with events
+carried in its dispatch (the phase breakdown); the timed region then runs K
+whole steps with events only on the dominant attention launch, whose average
+duration gives the roofline figure. ms_per_step is host wall time over the K
+steps, bracketed by device synchronisation.
 
 Work counts are algorithmic: F = sum 4 n L D Hq flops (QK^T and PV, no causal
 halving) and B = K/V read once per item + cache write of the fresh rows + Q
@@ -69,14 +69,16 @@ def cpu_baseline(wl, budget_s):
     def row_flops(i):
         return 4.0 * int(wl.kv_len[i]) * D * Hq
 
-    # calibrate the oracle's rate on a small piece of the workload
-    first = dec[0] if dec else pre[0]
-    call = oracle.Call(wl, [first])
-    cal_rows = {first: np.arange(min(wl.n(first), 8))}
+    # calibrate the oracle's rate on a piece of the workload large enough to
+    # keep every thread busy (a few whole block decodes, or 64 prefill rows)
+    cal_items = dec[:4] if dec else pre[:1]
+    cal_rows = {i: np.arange(wl.n(i) if wl.n(i) <= 32 else min(wl.n(i), 64)) for i in cal_items}
+    call = oracle.Call(wl, sorted(cal_rows))
     sel, _, _ = oracle.selection(call, cal_rows)
     t = time.perf_counter()
     oracle.run(call, sel)
-    rate = len(cal_rows[first]) * row_flops(first) / max(time.perf_counter() - t, 1e-6)
+    cal_flops = sum(len(r) * row_flops(i) for i, r in cal_rows.items())
+    rate = cal_flops / max(time.perf_counter() - t, 1e-6)
     target = rate * budget_s
 
     rows, acc = {}, 0.0
@@ -183,13 +185,14 @@ def main():
               t["page_ids"].data_ptr(), out.data_ptr(), lse.data_ptr(), ws.data_ptr(), ws.numel(),
               stream.cuda_stream]
 
-    def make_events(which=range(4)):
-        """Four event slots; slots outside `which` stay NULL (nothing recorded)."""
-        evs = [torch.cuda.Event(enable_timing=True) if j in which else None for j in range(4)]
+    def make_events(which=range(3)):
+        """Start / stop event pairs of the three launches; launches outside
+        `which` get NULL entries (no timestamps)."""
+        evs = [torch.cuda.Event(enable_timing=True) if j // 2 in which else None for j in range(6)]
         for e in evs:
             if e is not None:
                 e.record(stream)  # creates the HIP event
-        arr = (ctypes.c_void_p * 4)(*[e.cuda_event if e is not None else None for e in evs])
+        arr = (ctypes.c_void_p * 6)(*[e.cuda_event if e is not None else None for e in evs])
         return evs, arr
 
     flush_buf = torch.empty((512 << 20,), dtype=torch.uint8, device=dev) if args.flush else None
@@ -206,7 +209,7 @@ def main():
     torch.cuda.synchronize()
     print(f"[bench] warmup done ({args.warmup} steps)", file=sys.stderr, flush=True)
 
-    # phase breakdown, outside the timed region: events between all three launches
+    # phase breakdown, outside the timed region: events on all three launches
     K = args.steps
     n_phase = max(3, min(K, 10))
     evsets = [make_events() for _ in range(n_phase)]
@@ -218,14 +221,14 @@ def main():
     torch.cuda.synchronize()
     phase_ms = {}
     for j, name in enumerate(PHASES):
-        phase_ms[name] = float(np.mean([evsets[k][0][j].elapsed_time(evsets[k][0][j + 1])
+        phase_ms[name] = float(np.mean([evsets[k][0][2 * j].elapsed_time(evsets[k][0][2 * j + 1])
                                         for k in range(n_phase)]))
     work = split_work(wl, fused_decodes=int(p.info.num_fused_decode_tiles) > 0)
     dom = max(("prefill_attn", "decode_attn"), key=lambda n: phase_ms[n] if work[n][0] > 0 else -1)
     jd = PHASES.index(dom)
 
-    # timed region: K whole steps; only the dominant kernel is bracketed by events
-    evsets = [make_events((jd, jd + 1)) for _ in range(K)]
+    # timed region: K whole steps; only the dominant launch carries events
+    evsets = [make_events((jd,)) for _ in range(K)]
     torch.cuda.synchronize()
     if args.flush:
         step_ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
@@ -244,7 +247,7 @@ def main():
             check(lib.sangam_attn_forward_timed(*args_c, evsets[k][1]))
         torch.cuda.synchronize()
         ms_per_step = (time.perf_counter() - w0) * 1e3 / K
-    dom_ms = float(np.mean([evsets[k][0][jd].elapsed_time(evsets[k][0][jd + 1]) for k in range(K)]))
+    dom_ms = float(np.mean([evsets[k][0][2 * jd].elapsed_time(evsets[k][0][2 * jd + 1]) for k in range(K)]))
     print(f"[bench] timed {K} steps: {ms_per_step:.4f} ms/step", file=sys.stderr, flush=True)
 
     F, B = wl.flops(), wl.hbm_bytes()

@@ -140,16 +140,17 @@ sangam_status sangam_attn_forward(const void *plan_host, const void *plan_dev, c
                                   void *stream);
 
 /*
- * sangam_attn_forward, plus HIP events recorded on `stream` around its
- * launches, for measuring each kernel in place: events[0] before the
- * prefill-shaped attention launch, [1] before the decode-shaped launch, [2]
- * before the split merge, [3] after it (the KV write-back runs inside the two
- * attention launches). A launch with no work records its two events back to
- * back. events holds four entries, each a hipEvent_t the caller created (and
- * owns) or NULL to record nothing at that point (an event costs a few
- * microseconds of stream time, so a caller timing one kernel passes only the
- * two around it); otherwise identical to sangam_attn_forward. Errors: as
- * sangam_attn_forward, plus SANGAM_ERR_INVALID_ARG for a NULL events array.
+ * sangam_attn_forward, plus HIP events carried by its launches, for measuring
+ * each kernel in place: events[0] and [1] are the start and stop of the
+ * prefill-shaped attention launch, [2] and [3] of the decode-shaped launch,
+ * [4] and [5] of the split merge (the KV write-back runs inside the two
+ * attention launches). The events travel in the kernel dispatch itself, so
+ * their elapsed time is the kernel's execution time, as a kernel trace
+ * reports it. A launch with no work records its two events back to back.
+ * events holds six entries, each a hipEvent_t the caller created (and owns)
+ * or NULL for no timestamp; otherwise identical to sangam_attn_forward.
+ * Errors: as sangam_attn_forward, plus SANGAM_ERR_INVALID_ARG for a NULL
+ * events array.
  */
 sangam_status sangam_attn_forward_timed(const void *plan_host, const void *plan_dev,
                                         const void *q, const void *k_new, const void *v_new,

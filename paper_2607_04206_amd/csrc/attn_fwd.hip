@@ -23,6 +23,7 @@
 //                     into XOR-swizzled tiles (double buffered); V^T operands
 //                     come from ds_read_b64_tr_b16 transposing reads.
 //   merge_kernel      combines split-context partial (O, LSE) in split order.
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
 #include <string>
@@ -615,28 +616,43 @@ __global__ __launch_bounds__(256) void merge_kernel(MergeArgs a) {
 }
 
 // ------------------------------------------------------------------ launch
+// Start / stop events attached to one launch (timed entry point), or none.
+struct LaunchEvents {
+    hipEvent_t start = nullptr;
+    hipEvent_t stop = nullptr;
+};
+
+// A launch with events carries them in its dispatch (hipExtLaunchKernel), so
+// their timestamps bracket the kernel itself, as a kernel trace does.
+template <typename Args>
+hipError_t launch(const void* fn, unsigned blocks, unsigned threads, Args args, hipStream_t stream,
+                  LaunchEvents ev) {
+    void* kargs[] = {&args};
+    if (!ev.start && !ev.stop) return hipLaunchKernel(fn, dim3(blocks), dim3(threads), kargs, 0, stream);
+    return hipExtLaunchKernel(fn, dim3(blocks), dim3(threads), kargs, 0, stream, ev.start, ev.stop, 0);
+}
+
 template <int D, int QW, int KW, int QB, int NB, bool HA, int NSTAGE = 2>
-hipError_t launch_tiles(const AttnArgs& args, int n_tiles, hipStream_t stream) {
+hipError_t launch_tiles(const AttnArgs& args, int n_tiles, hipStream_t stream, LaunchEvents ev) {
     constexpr int MINB = min_blocks_per_cu<D, QW, KW, QB, NB, NSTAGE>();
-    attn_tiles_kernel<D, QW, KW, QB, NB, NSTAGE, HA, MINB>
-        <<<dim3(n_tiles), dim3(64 * QW * KW), 0, stream>>>(args);
-    return hipGetLastError();
+    return launch(reinterpret_cast<const void*>(&attn_tiles_kernel<D, QW, KW, QB, NB, NSTAGE, HA, MINB>),
+                  unsigned(n_tiles), unsigned(64 * QW * KW), args, stream, ev);
 }
 
 template <int D>
 hipError_t launch_decode(const AttnArgs& args, int n_tiles, int qw, int kw, int nb, hipStream_t stream,
-                         bool* supported) {
+                         LaunchEvents ev, bool* supported) {
     *supported = true;
-    if (qw == 1 && kw == 2 && nb == 1) return launch_tiles<D, 1, 2, 1, 1, true>(args, n_tiles, stream);
-    if (qw == 2 && kw == 2 && nb == 2) return launch_tiles<D, 2, 2, 1, 2, true>(args, n_tiles, stream);
+    if (qw == 1 && kw == 2 && nb == 1) return launch_tiles<D, 1, 2, 1, 1, true>(args, n_tiles, stream, ev);
+    if (qw == 2 && kw == 2 && nb == 2) return launch_tiles<D, 2, 2, 1, 2, true>(args, n_tiles, stream, ev);
     if (kw == 1 && nb == 2) {
         switch (qw) {
-            case 3: return launch_tiles<D, 3, 1, 1, 2, true>(args, n_tiles, stream);
-            case 4: return launch_tiles<D, 4, 1, 1, 2, true>(args, n_tiles, stream);
-            case 5: return launch_tiles<D, 5, 1, 1, 2, true>(args, n_tiles, stream);
-            case 6: return launch_tiles<D, 6, 1, 1, 2, true>(args, n_tiles, stream);
-            case 7: return launch_tiles<D, 7, 1, 1, 2, true>(args, n_tiles, stream);
-            case 8: return launch_tiles<D, 8, 1, 1, 2, true>(args, n_tiles, stream);
+            case 3: return launch_tiles<D, 3, 1, 1, 2, true>(args, n_tiles, stream, ev);
+            case 4: return launch_tiles<D, 4, 1, 1, 2, true>(args, n_tiles, stream, ev);
+            case 5: return launch_tiles<D, 5, 1, 1, 2, true>(args, n_tiles, stream, ev);
+            case 6: return launch_tiles<D, 6, 1, 1, 2, true>(args, n_tiles, stream, ev);
+            case 7: return launch_tiles<D, 7, 1, 1, 2, true>(args, n_tiles, stream, ev);
+            case 8: return launch_tiles<D, 8, 1, 1, 2, true>(args, n_tiles, stream, ev);
             default: break;
         }
     }
@@ -685,11 +701,24 @@ static sangam_status forward_impl(const void* plan_host, const void* plan_dev, c
     }
     hipStream_t stream = static_cast<hipStream_t>(stream_ptr);
     const uint8_t* pd = static_cast<const uint8_t*>(plan_dev);
-    auto mark = [&](int k) -> hipError_t {
-        return events && events[k] ? hipEventRecord(static_cast<hipEvent_t>(events[k]), stream) : hipSuccess;
+    // events[2k], events[2k+1] bracket launch k (prefill-shaped, decode-shaped,
+    // merge); a launch with no work records its pair back to back
+    auto evs = [&](int k) {
+        LaunchEvents ev;
+        if (events) {
+            ev.start = static_cast<hipEvent_t>(events[2 * k]);
+            ev.stop = static_cast<hipEvent_t>(events[2 * k + 1]);
+        }
+        return ev;
+    };
+    auto mark_empty = [&](int k) -> hipError_t {
+        const LaunchEvents ev = evs(k);
+        for (hipEvent_t e : {ev.start, ev.stop})
+            if (e)
+                if (hipError_t r = hipEventRecord(e, stream); r != hipSuccess) return r;
+        return hipSuccess;
     };
     const ItemRec* items = reinterpret_cast<const ItemRec*>(pd + h->off_items);
-    if (hipError_t e = mark(0); e != hipSuccess) return hip_fail(e, "event record");
 
     AttnArgs args{nullptr,
                   items,
@@ -710,26 +739,29 @@ static sangam_status forward_impl(const void* plan_host, const void* plan_dev, c
     // decode-shaped tiles; both also write the fresh rows into their pages
     if (h->n_prefill_tiles > 0) {
         args.tiles = reinterpret_cast<const TileRec*>(pd + h->off_prefill_tiles);
-        hipError_t e = h->d == 128
-                           ? launch_tiles<128, kPrefillQWaves, 1, kPrefillQBlocks, 2, false>(args, h->n_prefill_tiles, stream)
-                           : launch_tiles<64, kPrefillQWaves, 1, kPrefillQBlocks, 2, false>(args, h->n_prefill_tiles, stream);
+        hipError_t e =
+            h->d == 128
+                ? launch_tiles<128, kPrefillQWaves, 1, kPrefillQBlocks, 2, false>(args, h->n_prefill_tiles, stream, evs(0))
+                : launch_tiles<64, kPrefillQWaves, 1, kPrefillQBlocks, 2, false>(args, h->n_prefill_tiles, stream, evs(0));
         if (e != hipSuccess) return hip_fail(e, "prefill attention launch");
+    } else if (hipError_t e = mark_empty(0); e != hipSuccess) {
+        return hip_fail(e, "event record");
     }
-    if (hipError_t e = mark(1); e != hipSuccess) return hip_fail(e, "event record");
     if (h->n_decode_tiles > 0) {
         args.tiles = reinterpret_cast<const TileRec*>(pd + h->off_decode_tiles);
         bool ok = false;
         hipError_t e = h->d == 128 ? launch_decode<128>(args, h->n_decode_tiles, h->decode_qw, h->decode_kw,
-                                                        h->decode_nb, stream, &ok)
+                                                        h->decode_nb, stream, evs(1), &ok)
                                    : launch_decode<64>(args, h->n_decode_tiles, h->decode_qw, h->decode_kw,
-                                                       h->decode_nb, stream, &ok);
+                                                       h->decode_nb, stream, evs(1), &ok);
         if (!ok) {
             set_error("no decode kernel for this head grouping");
             return SANGAM_ERR_UNSUPPORTED;
         }
         if (e != hipSuccess) return hip_fail(e, "decode attention launch");
+    } else if (hipError_t e = mark_empty(1); e != hipSuccess) {
+        return hip_fail(e, "event record");
     }
-    if (hipError_t e = mark(2); e != hipSuccess) return hip_fail(e, "event record");
 
     // 2. merge split contexts
     if (h->n_merge_rows > 0) {
@@ -740,11 +772,12 @@ static sangam_status forward_impl(const void* plan_host, const void* plan_dev, c
                     lse,
                     h->hq,
                     h->d};
-        merge_kernel<<<dim3(unsigned(h->n_merge_rows)), dim3(256), 0, stream>>>(m);
-        hipError_t e = hipGetLastError();
+        hipError_t e = launch(reinterpret_cast<const void*>(&merge_kernel), unsigned(h->n_merge_rows), 256u, m,
+                              stream, evs(2));
         if (e != hipSuccess) return hip_fail(e, "merge launch");
+    } else if (hipError_t e = mark_empty(2); e != hipSuccess) {
+        return hip_fail(e, "event record");
     }
-    if (hipError_t e = mark(3); e != hipSuccess) return hip_fail(e, "event record");
     return SANGAM_OK;
 }
 

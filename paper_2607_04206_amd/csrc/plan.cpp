@@ -65,8 +65,11 @@ static int decode_kv_waves(int qw) {
 // Shortest context chunk the planner cuts for balance (forced splits above
 // kForcedSplitLen aside): a chunk must carry enough keys to amortize a
 // work-group's prologue and its merge traffic. A GQA work-group does G times
-// the work per key, so it tolerates shorter chunks.
-static int64_t min_chunk(int qw) { return qw == 1 ? 2048 : 512; }
+// the work per key, so it tolerates shorter chunks; but each of its chunks
+// also writes (and the merge reads back) a G x 32-row fp32 partial, which
+// below about 1024 keys costs more than the balance gains (measured on
+// block decodes of 28/4 heads).
+static int64_t min_chunk(int qw) { return qw == 1 ? 2048 : 1024; }
 
 const PlanHeader* check_plan(const void* plan) {
     if (!plan) return nullptr;
