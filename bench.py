@@ -131,6 +131,69 @@ def measured_traffic(workload, kernel):
     return None if k is None else k.get("hbm_bytes_per_launch")
 
 
+def decode_sweep(args):
+    """Decode iteration time against batch size (the attention-only analogue
+    of the paper's decode-batch measurement): each point is one call over B
+    block decodes at L = 1024, timed over `steps` back-to-back calls; the
+    dominant launch is timed with dispatch-attached events."""
+    import ctypes
+    import numpy as np
+    import torch
+
+    import workloads
+    from paper_2607_04206_amd import attn
+    from paper_2607_04206_amd._lib import check, lib
+
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream(dev)
+    for shape in ("llada", "dream"):
+        for B in (1, 2, 4, 8, 16, 32, 64):
+            wl = workloads.decode_sweep(shape, B, args.seed)
+            t = workloads.device_inputs(wl, dev, fill=None)
+            p = attn.plan(q_indptr=wl.q_indptr, q_offset=wl.q_offset, kv_len=wl.kv_len,
+                          page_indptr=wl.page_indptr, page_ids=wl.page_ids,
+                          num_q_heads=wl.num_q_heads, num_kv_heads=wl.num_kv_heads,
+                          head_dim=wl.head_dim, num_pool_pages=wl.num_pool_pages,
+                          sm_scale=wl.sm_scale, device=dev)
+            out = torch.empty((wl.total_q, wl.num_q_heads, wl.head_dim), dtype=torch.bfloat16, device=dev)
+            lse = torch.empty((wl.total_q, wl.num_q_heads), dtype=torch.float32, device=dev)
+            ws = torch.empty((max(p.workspace_bytes, 16),), dtype=torch.uint8, device=dev)
+            args_c = [p.host_ptr(), p.dev.data_ptr(), t["q"].data_ptr(), t["k_new"].data_ptr(),
+                      t["v_new"].data_ptr(), t["k_cache"].data_ptr(), t["v_cache"].data_ptr(),
+                      t["page_ids"].data_ptr(), out.data_ptr(), lse.data_ptr(), ws.data_ptr(), ws.numel(),
+                      stream.cuda_stream]
+            for _ in range(args.warmup):
+                check(lib.sangam_attn_forward(*args_c))
+            K = args.steps
+            evs = []
+            for _ in range(K):
+                e = [torch.cuda.Event(enable_timing=True) for _ in range(6)]
+                for x in e:
+                    x.record(stream)
+                evs.append((e, (ctypes.c_void_p * 6)(*[x.cuda_event for x in e])))
+            torch.cuda.synchronize()
+            w0 = time.perf_counter()
+            for k in range(K):
+                check(lib.sangam_attn_forward(*args_c))
+            torch.cuda.synchronize()
+            ms = (time.perf_counter() - w0) * 1e3 / K
+            for k in range(K):
+                check(lib.sangam_attn_forward_timed(*args_c, evs[k][1]))
+            torch.cuda.synchronize()
+            launches = np.mean([[e[2 * j].elapsed_time(e[2 * j + 1]) for j in range(3)] for e, _ in evs], 0)
+            F, Bytes = wl.flops(), wl.hbm_bytes()
+            kern = float(launches[1])  # the decode-shaped launch (no prefill in the batch)
+            print(json.dumps({
+                "sweep": "decode_batch", "shape": shape, "num_q_heads": wl.num_q_heads,
+                "num_kv_heads": wl.num_kv_heads, "batch": B, "kv_len": 1024, "ms_per_call": ms,
+                "decode_kernel_ms": kern, "merge_ms": float(launches[2]),
+                "tflops": F / (ms / 1e3) / 1e12, "hbm_gbs": Bytes / (ms / 1e3) / 1e9,
+                "kernel_hbm_frac": Bytes / (kern / 1e3) / (PEAK_HBM_GBS * 1e9),
+                "kernel_mfma_frac": F / (kern / 1e3) / (PEAK_BF16_TFLOPS * 1e12),
+                "splits": int(p.info.num_split_items), "tiles": int(p.info.num_decode_tiles)}), flush=True)
+            del t, out, lse, ws
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -144,6 +207,9 @@ def main():
     ap.add_argument("--copy-calib-mib", type=int, default=0,
                     help="run one device-to-device copy of this many MiB before warm-up, as the "
                          "reference kernel that scales the HBM traffic counters")
+    ap.add_argument("--decode-sweep", action="store_true",
+                    help="instead of one workload: block-decode batches of 1..64 requests at L = 1024 "
+                         "for the LLaDA (32/32) and Dream (28/4) head shapes, one JSON line each")
     ap.add_argument("--flush", action="store_true",
                     help="overwrite 512 MiB between steps (outside the timing) so no step reads "
                          "the previous one's data from the 256 MB Infinity Cache; steps are then "
@@ -154,6 +220,9 @@ def main():
         print("bench.py measures one GPU only: this build has no multi-GPU path "
               "(run with --gpus 1).", file=sys.stderr)
         sys.exit(2)
+    if args.decode_sweep:
+        decode_sweep(args)
+        return
 
     import numpy as np
     import torch

@@ -583,36 +583,37 @@ struct MergeArgs {
     int32_t d;
 };
 
+// grid: (merge row, 256-element slice of the row's Hq x D/4 float4 outputs);
+// one thread per float4 of one head, so that every partial of a row is
+// loaded by a different thread in parallel
 __global__ __launch_bounds__(256) void merge_kernel(MergeArgs a) {
     const MergeRow mr = a.rows[blockIdx.x];
     const ItemRec it = a.items[mr.item];
     const int S = it.num_splits;
     const int d4n = a.d / 4;
-    for (int e = threadIdx.x; e < a.hq * d4n; e += 256) {
-        const int head = e / d4n;
-        const int d4 = e - head * d4n;
-        float mx = -INFINITY;
-        for (int s = 0; s < S; ++s)
-            mx = fmaxf(mx, a.ws[it.ws_lse + (size_t)(s * it.n + mr.row) * a.hq + head]);
-        float tot = 0.0f;
-        float4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
-        for (int s = 0; s < S; ++s) {
-            const size_t prow = (size_t)(s * it.n + mr.row) * a.hq + head;
-            const float w = __expf(a.ws[it.ws_lse + prow] - mx);
-            const float4 v = *(const float4*)(a.ws + it.ws_o + prow * a.d + 4 * d4);
-            tot += w;
-            acc.x += w * v.x;
-            acc.y += w * v.y;
-            acc.z += w * v.z;
-            acc.w += w * v.w;
-        }
-        const float inv = 1.0f / tot;
-        const bf16x4 v = {(__bf16)(acc.x * inv), (__bf16)(acc.y * inv), (__bf16)(acc.z * inv),
-                          (__bf16)(acc.w * inv)};
-        const size_t orow = (size_t)(it.q_start + mr.row) * a.hq + head;
-        *(u32x2*)(a.out + orow * a.d + 4 * d4) = __builtin_bit_cast(u32x2, v);
-        if (d4 == 0 && a.lse) a.lse[orow] = mx + logf(tot);
+    const int e = blockIdx.y * 256 + threadIdx.x;
+    if (e >= a.hq * d4n) return;
+    const int head = e / d4n;
+    const int d4 = e - head * d4n;
+    float mx = -INFINITY;
+    for (int s = 0; s < S; ++s) mx = fmaxf(mx, a.ws[it.ws_lse + (size_t)(s * it.n + mr.row) * a.hq + head]);
+    float tot = 0.0f;
+    float4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
+    for (int s = 0; s < S; ++s) {
+        const size_t prow = (size_t)(s * it.n + mr.row) * a.hq + head;
+        const float w = __expf(a.ws[it.ws_lse + prow] - mx);
+        const float4 v = *(const float4*)(a.ws + it.ws_o + prow * a.d + 4 * d4);
+        tot += w;
+        acc.x += w * v.x;
+        acc.y += w * v.y;
+        acc.z += w * v.z;
+        acc.w += w * v.w;
     }
+    const float inv = 1.0f / tot;
+    const bf16x4 v = {(__bf16)(acc.x * inv), (__bf16)(acc.y * inv), (__bf16)(acc.z * inv), (__bf16)(acc.w * inv)};
+    const size_t orow = (size_t)(it.q_start + mr.row) * a.hq + head;
+    *(u32x2*)(a.out + orow * a.d + 4 * d4) = __builtin_bit_cast(u32x2, v);
+    if (d4 == 0 && a.lse) a.lse[orow] = mx + logf(tot);
 }
 
 // ------------------------------------------------------------------ launch
@@ -625,18 +626,17 @@ struct LaunchEvents {
 // A launch with events carries them in its dispatch (hipExtLaunchKernel), so
 // their timestamps bracket the kernel itself, as a kernel trace does.
 template <typename Args>
-hipError_t launch(const void* fn, unsigned blocks, unsigned threads, Args args, hipStream_t stream,
-                  LaunchEvents ev) {
+hipError_t launch(const void* fn, dim3 grid, unsigned threads, Args args, hipStream_t stream, LaunchEvents ev) {
     void* kargs[] = {&args};
-    if (!ev.start && !ev.stop) return hipLaunchKernel(fn, dim3(blocks), dim3(threads), kargs, 0, stream);
-    return hipExtLaunchKernel(fn, dim3(blocks), dim3(threads), kargs, 0, stream, ev.start, ev.stop, 0);
+    if (!ev.start && !ev.stop) return hipLaunchKernel(fn, grid, dim3(threads), kargs, 0, stream);
+    return hipExtLaunchKernel(fn, grid, dim3(threads), kargs, 0, stream, ev.start, ev.stop, 0);
 }
 
 template <int D, int QW, int KW, int QB, int NB, bool HA, int NSTAGE = 2>
 hipError_t launch_tiles(const AttnArgs& args, int n_tiles, hipStream_t stream, LaunchEvents ev) {
     constexpr int MINB = min_blocks_per_cu<D, QW, KW, QB, NB, NSTAGE>();
     return launch(reinterpret_cast<const void*>(&attn_tiles_kernel<D, QW, KW, QB, NB, NSTAGE, HA, MINB>),
-                  unsigned(n_tiles), unsigned(64 * QW * KW), args, stream, ev);
+                  dim3(unsigned(n_tiles)), unsigned(64 * QW * KW), args, stream, ev);
 }
 
 template <int D>
@@ -772,8 +772,9 @@ static sangam_status forward_impl(const void* plan_host, const void* plan_dev, c
                     lse,
                     h->hq,
                     h->d};
-        hipError_t e = launch(reinterpret_cast<const void*>(&merge_kernel), unsigned(h->n_merge_rows), 256u, m,
-                              stream, evs(2));
+        const unsigned slices = unsigned((h->hq * (h->d / 4) + 255) / 256);
+        hipError_t e = launch(reinterpret_cast<const void*>(&merge_kernel), dim3(unsigned(h->n_merge_rows), slices),
+                              256u, m, stream, evs(2));
         if (e != hipSuccess) return hip_fail(e, "merge launch");
     } else if (hipError_t e = mark_empty(2); e != hipSuccess) {
         return hip_fail(e, "event record");

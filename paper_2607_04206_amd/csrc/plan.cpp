@@ -70,6 +70,8 @@ static int decode_kv_waves(int qw) {
 // below about 1024 keys costs more than the balance gains (measured on
 // block decodes of 28/4 heads).
 static int64_t min_chunk(int qw) { return qw == 1 ? 2048 : 1024; }
+// the same floor while a decode launch leaves CUs idle (see below)
+static int64_t min_chunk_idle(int qw) { return qw == 1 ? 256 : 512; }
 
 const PlanHeader* check_plan(const void* plan) {
     if (!plan) return nullptr;
@@ -165,13 +167,23 @@ extern "C" sangam_status sangam_attn_plan(const sangam_attn_desc* d, void* plan_
         has_prefill = int64_t(d->q_indptr[i + 1]) - d->q_indptr[i] > kWaveRows;
     const bool fuse = has_prefill && G >= kPrefillQWaves;
     const int fused_tiles_per_kv_head = int(ceil_div(G, kPrefillQWaves));
-    int64_t decode_keys = 0;
+    int64_t decode_keys = 0, decode_units = 0;
     for (int i = 0; i < n_items; ++i) {
         const int64_t n = int64_t(d->q_indptr[i + 1]) - d->q_indptr[i];
-        if (n <= kWaveRows && !fuse) decode_keys += int64_t(hkv) * tiles_per_kv_head * d->kv_len[i];
+        if (n <= kWaveRows && !fuse) {
+            decode_keys += int64_t(hkv) * tiles_per_kv_head * d->kv_len[i];
+            decode_units += int64_t(hkv) * tiles_per_kv_head;
+        }
     }
+    // While the unsplit decode work-groups would leave CUs idle (a small
+    // batch: fewer than two MHA work-groups, or one GQA work-group, per CU),
+    // a call is bound by the latency of each work-group's stage chain, not by
+    // bandwidth: then chunks go down to min_chunk_idle keys, at a merge cost
+    // that stays small in absolute terms.
+    const bool underfilled = decode_units < int64_t(num_cus) * (qw == 1 ? 2 : 1);
     int64_t chunk = ceil_div(decode_keys, 4 * int64_t(num_cus));
-    chunk = std::min<int64_t>(std::max<int64_t>(round_up(std::max<int64_t>(chunk, 1), kKeyAlign), min_chunk(qw)),
+    chunk = std::min<int64_t>(std::max<int64_t>(round_up(std::max<int64_t>(chunk, 1), kKeyAlign),
+                                                underfilled ? min_chunk_idle(qw) : min_chunk(qw)),
                               kForcedSplitLen);
 
     std::vector<ItemRec> items(n_items);

@@ -223,6 +223,16 @@ def test_long_decode(dev):
     check_pool_untouched(wl, t)
 
 
+@pytest.mark.parametrize("shape", ["llada", "dream"])
+@pytest.mark.parametrize("batch", [1, 64])
+def test_decode_sweep_points(dev, shape, batch):
+    """End points of the decode-batch sweep (block decodes at L = 1024)."""
+    wl = workloads.decode_sweep(shape, batch, seed=1)
+    p, t, out, lse = run(wl, dev)
+    check_full(wl, out, lse)
+    check_cache(wl, t)
+
+
 def test_deterministic(dev):
     wl = workloads.dream_mixed(1)
     _, _, o1, l1 = run(wl, dev)

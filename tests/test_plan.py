@@ -296,3 +296,29 @@ def test_long_decode_plan_is_fast_and_sized():
     assert len(pre) == 0
     assert np.all(items["split_len"] <= 8192)
     assert np.all((items["L"] <= 8192) | (items["num_splits"] >= 2))
+
+
+def test_decode_sweep_workloads():
+    # decode-batch sweep points: B block decodes of 32 rows at L = 1024, block
+    # index in the last 256 positions
+    for shape in workloads.SWEEP_SHAPES:
+        for B in (1, 64):
+            wl = workloads.decode_sweep(shape, B)
+            assert wl.num_items == B and (wl.kv_len == 1024).all()
+            assert (np.diff(wl.q_indptr) == 32).all()
+            assert ((wl.q_offset >= 768) & (wl.q_offset <= 992) & (wl.q_offset % 32 == 0)).all()
+
+
+def test_underfilled_decode_launch_splits_finer():
+    # fewer decode work-groups than two per CU: contexts are cut down to
+    # 256-key chunks; a full launch keeps MHA chunks of at least 2048 keys
+    small = plan_of(workloads.decode_sweep("llada", 1))
+    h, items, dec, pre, mer = parse(small)
+    assert len(pre) == 0 and items["num_splits"][0] == 4 and items["split_len"][0] == 256
+    assert len(dec) == 32 * 4 and len(mer) == 32
+    full = plan_of(workloads.decode_sweep("llada", 64))
+    h, items, dec, pre, mer = parse(full)
+    assert (items["num_splits"] == 1).all() and len(dec) == 64 * 32 and len(mer) == 0
+    # the same batch on a 16-CU part counts as full
+    h, items, dec, pre, mer = parse(plan_of(workloads.decode_sweep("llada", 1), num_cus=16))
+    assert (items["num_splits"] == 1).all()

@@ -354,6 +354,21 @@ CONFIGS = {
 }
 
 
+SWEEP_SHAPES = {"llada": (32, 32), "dream": (28, 4)}
+
+
+def decode_sweep(shape: str, batch: int, seed: int = 0, L: int = 1024) -> Workload:
+    """Decode-batch sweep point: `batch` block decodes of one model shape (LLaDA
+    32/32 or Dream 28/4 heads, D 128), every request with L = 1024 cached
+    positions and its 32-row block at a random block index of the last 256."""
+    hq, hkv = SWEEP_SHAPES[shape]
+    rng = np.random.default_rng(seed)
+    blocks = rng.integers(0, 8, size=batch)
+    dec = [(L - 256 + 32 * int(b), L) for b in blocks]
+    return make_workload(f"decode_sweep_{shape}_{batch}", seed, hq=hq, hkv=hkv, d=128, decodes=dec,
+                         prefills=[], rng=rng)
+
+
 def by_index(idx: int, seed: int = 0) -> Workload:
     return CONFIGS[idx](seed)
 
