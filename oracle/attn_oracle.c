@@ -15,6 +15,11 @@
  *     recomputes only its own block (Sec. 2.2, blockwise Fast-dLLM cache):
  *     positions [o, o+n) take the fresh rows k_new / v_new, all others come
  *     from the cache as it stood before the call.
+ *   - A per-token cached decode (Sec. 2.2, the dKV-Cache-PD variant: prompt
+ *     KV fixed, response tokens refreshed individually) recomputes an
+ *     arbitrary set of positions: when a position list q_pos is given, row r
+ *     of an item sits at position q_pos[r] instead of o + r; every other rule
+ *     is the same.
  *   - A prefill brings its whole sequence as fresh rows (o = 0, n = L) and
  *     refreshes the cache with them (Sec. 2.2; whole, never chunked, Sec. 3.2).
  *   - Per (item, query row r, query head h), with G = Hq / Hkv and the KV head
@@ -51,46 +56,86 @@ static double widen(uint16_t h)
 
 typedef struct {
     int32_t n_items, hq, hkv, d;
-    const int32_t *q_indptr, *q_offset, *kv_len;
+    const int32_t *q_indptr, *q_offset, *q_pos, *kv_len;
     const int64_t *ctx_indptr;
     const uint16_t *q, *k_new, *v_new, *k_ctx, *v_ctx;
+    /* fresh[seq_base[i] + j]: packed row that holds position j of item i, or
+     * -1 when position j comes from the pre-call cache */
+    int64_t *seq_base, *fresh;
 } call_t;
+
+/* position of local row r of item i */
+static int64_t row_pos(const call_t *c, int32_t i, int64_t r)
+{
+    return c->q_pos ? c->q_pos[c->q_indptr[i] + r] : c->q_offset[i] + r;
+}
 
 /*
  * Row j (position in [0, L)) of the assembled key (or value) sequence of item
- * i for KV head g: the fresh row when o <= j < o + n, else the pre-call cache.
+ * i for KV head g: the fresh row that sits at position j, else the pre-call
+ * cache.
  */
 static const uint16_t *seq_row(const call_t *c, int32_t i, int64_t j, int32_t g, int value)
 {
-    int64_t o = c->q_offset[i];
-    int64_t n = (int64_t)c->q_indptr[i + 1] - c->q_indptr[i];
-    if (j >= o && j < o + n) {
-        int64_t row = (int64_t)c->q_indptr[i] + (j - o);
+    int64_t row = c->fresh[c->seq_base[i] + j];
+    if (row >= 0) {
         const uint16_t *base = value ? c->v_new : c->k_new;
         return base + (row * c->hkv + g) * c->d;
     }
     const uint16_t *base = value ? c->v_ctx : c->k_ctx;
-    int64_t row = c->ctx_indptr[i] + j;
+    row = c->ctx_indptr[i] + j;
     return base + (row * c->hkv + g) * c->d;
 }
 
-static int check_call(const call_t *c)
+static void release(call_t *c)
 {
+    free(c->seq_base);
+    free(c->fresh);
+    c->seq_base = c->fresh = NULL;
+}
+
+/* validate the call and build the position -> fresh row map */
+static int check_call(call_t *c)
+{
+    c->seq_base = c->fresh = NULL;
     if (c->n_items < 0 || c->hq <= 0 || c->hkv <= 0 || c->d <= 0)
         return ORACLE_EINVAL;
     if (c->hq % c->hkv != 0)
         return ORACLE_EINVAL;
+    int64_t total = 0;
     for (int32_t i = 0; i < c->n_items; ++i) {
         int64_t n = (int64_t)c->q_indptr[i + 1] - c->q_indptr[i];
-        int64_t o = c->q_offset[i], L = c->kv_len[i];
+        int64_t L = c->kv_len[i];
         int64_t ctx = c->ctx_indptr[i + 1] - c->ctx_indptr[i];
-        if (n < 1 || o < 0 || o + n > L)
+        if (n < 1 || L < 1)
             return ORACLE_EINVAL;
+        /* positions strictly increasing inside [0, L) */
+        for (int64_t r = 0; r < n; ++r) {
+            int64_t p = row_pos(c, i, r);
+            if (p < 0 || p >= L || (r > 0 && p <= row_pos(c, i, r - 1)))
+                return ORACLE_EINVAL;
+        }
         /* an item without pre-call context must bring every row fresh */
-        if (ctx == 0 && !(o == 0 && n == L))
+        if (ctx == 0 && n != L)
             return ORACLE_EINVAL;
         if (ctx != 0 && ctx != L)
             return ORACLE_EINVAL;
+        total += L;
+    }
+    c->seq_base = (int64_t *)malloc(sizeof(int64_t) * (size_t)(c->n_items + 1));
+    c->fresh = (int64_t *)malloc(sizeof(int64_t) * (size_t)(total > 0 ? total : 1));
+    if (!c->seq_base || !c->fresh) {
+        release(c);
+        return ORACLE_ENOMEM;
+    }
+    c->seq_base[0] = 0;
+    for (int32_t i = 0; i < c->n_items; ++i) {
+        int64_t base = c->seq_base[i], L = c->kv_len[i];
+        for (int64_t j = 0; j < L; ++j)
+            c->fresh[base + j] = -1;
+        for (int64_t r = 0; r < (int64_t)c->q_indptr[i + 1] - c->q_indptr[i]; ++r)
+            c->fresh[base + row_pos(c, i, r)] = (int64_t)c->q_indptr[i] + r;
+        c->seq_base[i + 1] = base + L;
     }
     return ORACLE_OK;
 }
@@ -163,13 +208,13 @@ static int32_t item_of_row(const call_t *c, int64_t r)
  * Returns 0, or a negative code for an invalid call.
  */
 int oracle_attn(int32_t n_items, int32_t hq, int32_t hkv, int32_t d, float sm_scale,
-                const int32_t *q_indptr, const int32_t *q_offset, const int32_t *kv_len,
-                const int64_t *ctx_indptr, const uint16_t *q, const uint16_t *k_new,
-                const uint16_t *v_new, const uint16_t *k_ctx, const uint16_t *v_ctx,
-                const int64_t *sel, int64_t n_sel, double *out, double *lse)
+                const int32_t *q_indptr, const int32_t *q_offset, const int32_t *q_pos,
+                const int32_t *kv_len, const int64_t *ctx_indptr, const uint16_t *q,
+                const uint16_t *k_new, const uint16_t *v_new, const uint16_t *k_ctx,
+                const uint16_t *v_ctx, const int64_t *sel, int64_t n_sel, double *out, double *lse)
 {
-    call_t c = {n_items, hq, hkv, d, q_indptr, q_offset, kv_len, ctx_indptr,
-                q, k_new, v_new, k_ctx, v_ctx};
+    call_t c = {n_items, hq, hkv, d, q_indptr, q_offset, q_pos, kv_len, ctx_indptr,
+                q, k_new, v_new, k_ctx, v_ctx, NULL, NULL};
     int rc = check_call(&c);
     if (rc)
         return rc;
@@ -180,8 +225,10 @@ int oracle_attn(int32_t n_items, int32_t hq, int32_t hkv, int32_t d, float sm_sc
         if (kv_len[i] > max_l)
             max_l = kv_len[i];
     for (int64_t s = 0; sel && s < count; ++s)
-        if (sel[s] < 0 || sel[s] >= total_rows * hq)
+        if (sel[s] < 0 || sel[s] >= total_rows * hq) {
+            release(&c);
             return ORACLE_EINVAL;
+        }
     const double sigma = (double)sm_scale;
     int failed = 0;
 
@@ -204,6 +251,7 @@ int oracle_attn(int32_t n_items, int32_t hq, int32_t hkv, int32_t d, float sm_sc
         }
         free(w);
     }
+    release(&c);
     return failed ? ORACLE_ENOMEM : ORACLE_OK;
 }
 
@@ -212,44 +260,51 @@ int oracle_attn(int32_t n_items, int32_t hq, int32_t hkv, int32_t d, float sm_sc
  * w_out must hold kv_len of the row's item.
  */
 int oracle_weights(int32_t n_items, int32_t hq, int32_t hkv, int32_t d, float sm_scale,
-                   const int32_t *q_indptr, const int32_t *q_offset, const int32_t *kv_len,
-                   const int64_t *ctx_indptr, const uint16_t *q, const uint16_t *k_new,
-                   const uint16_t *v_new, const uint16_t *k_ctx, const uint16_t *v_ctx,
-                   int64_t row, int32_t head, double *w_out)
+                   const int32_t *q_indptr, const int32_t *q_offset, const int32_t *q_pos,
+                   const int32_t *kv_len, const int64_t *ctx_indptr, const uint16_t *q,
+                   const uint16_t *k_new, const uint16_t *v_new, const uint16_t *k_ctx,
+                   const uint16_t *v_ctx, int64_t row, int32_t head, double *w_out)
 {
-    call_t c = {n_items, hq, hkv, d, q_indptr, q_offset, kv_len, ctx_indptr,
-                q, k_new, v_new, k_ctx, v_ctx};
+    call_t c = {n_items, hq, hkv, d, q_indptr, q_offset, q_pos, kv_len, ctx_indptr,
+                q, k_new, v_new, k_ctx, v_ctx, NULL, NULL};
     int rc = check_call(&c);
     if (rc)
         return rc;
-    if (row < 0 || row >= q_indptr[n_items] || head < 0 || head >= hq)
+    if (row < 0 || row >= q_indptr[n_items] || head < 0 || head >= hq) {
+        release(&c);
         return ORACLE_EINVAL;
+    }
     int32_t i = item_of_row(&c, row);
     one_row(&c, (double)sm_scale, i, row, head, w_out, NULL, NULL);
+    release(&c);
     return ORACLE_OK;
 }
 
 /*
  * The cache content of item i after the call: positions [0, L) with the fresh
- * rows written over [o, o+n). k_out / v_out: [L, hkv, d] bf16 bits.
+ * rows written over their positions. k_out / v_out: [L, hkv, d] bf16 bits.
  */
 int oracle_expected_kv(int32_t n_items, int32_t hkv, int32_t d, const int32_t *q_indptr,
-                       const int32_t *q_offset, const int32_t *kv_len, const int64_t *ctx_indptr,
-                       const uint16_t *k_new, const uint16_t *v_new, const uint16_t *k_ctx,
-                       const uint16_t *v_ctx, int32_t item, uint16_t *k_out, uint16_t *v_out)
+                       const int32_t *q_offset, const int32_t *q_pos, const int32_t *kv_len,
+                       const int64_t *ctx_indptr, const uint16_t *k_new, const uint16_t *v_new,
+                       const uint16_t *k_ctx, const uint16_t *v_ctx, int32_t item, uint16_t *k_out,
+                       uint16_t *v_out)
 {
-    call_t c = {n_items, hkv, hkv, d, q_indptr, q_offset, kv_len, ctx_indptr,
-                NULL, k_new, v_new, k_ctx, v_ctx};
+    call_t c = {n_items, hkv, hkv, d, q_indptr, q_offset, q_pos, kv_len, ctx_indptr,
+                NULL, k_new, v_new, k_ctx, v_ctx, NULL, NULL};
     int rc = check_call(&c);
     if (rc)
         return rc;
-    if (item < 0 || item >= n_items)
+    if (item < 0 || item >= n_items) {
+        release(&c);
         return ORACLE_EINVAL;
+    }
     for (int64_t j = 0; j < kv_len[item]; ++j)
         for (int32_t g = 0; g < hkv; ++g) {
             memcpy(k_out + (j * hkv + g) * d, seq_row(&c, item, j, g, 0), sizeof(uint16_t) * d);
             memcpy(v_out + (j * hkv + g) * d, seq_row(&c, item, j, g, 1), sizeof(uint16_t) * d);
         }
+    release(&c);
     return ORACLE_OK;
 }
 

@@ -40,11 +40,11 @@ def lib():
         L = ctypes.CDLL(LIB)
         P = ctypes.c_void_p
         i32, i64, f32 = ctypes.c_int32, ctypes.c_int64, ctypes.c_float
-        L.oracle_attn.argtypes = [i32, i32, i32, i32, f32, P, P, P, P, P, P, P, P, P, P, i64, P, P]
+        L.oracle_attn.argtypes = [i32, i32, i32, i32, f32, P, P, P, P, P, P, P, P, P, P, P, i64, P, P]
         L.oracle_attn.restype = ctypes.c_int
-        L.oracle_weights.argtypes = [i32, i32, i32, i32, f32, P, P, P, P, P, P, P, P, P, i64, i32, P]
+        L.oracle_weights.argtypes = [i32, i32, i32, i32, f32, P, P, P, P, P, P, P, P, P, P, i64, i32, P]
         L.oracle_weights.restype = ctypes.c_int
-        L.oracle_expected_kv.argtypes = [i32, i32, i32, P, P, P, P, P, P, P, P, i32, P, P]
+        L.oracle_expected_kv.argtypes = [i32, i32, i32, P, P, P, P, P, P, P, P, P, i32, P, P]
         L.oracle_expected_kv.restype = ctypes.c_int
         L.oracle_threads.argtypes = [ctypes.c_int]
         L.oracle_threads.restype = ctypes.c_int
@@ -77,6 +77,10 @@ class Call:
         self.q_indptr = np.zeros(len(n) + 1, np.int32)
         self.q_indptr[1:] = np.cumsum(n)
         self.q_offset = np.asarray([wl.q_offset[i] for i in self.items], np.int32)
+        # per-row positions (None: rows of item i sit at q_offset[i] + r)
+        self.q_pos = None
+        if getattr(wl, "q_pos", None) is not None:
+            self.q_pos = np.concatenate([wl.positions(i) for i in self.items]).astype(np.int32)
         self.kv_len = np.asarray([wl.kv_len[i] for i in self.items], np.int32)
         z = np.zeros((0,), np.uint16)
         empty = (lambda: z)
@@ -98,7 +102,8 @@ class Call:
 
     def args(self):
         return (len(self.items), self.hq, self.hkv, self.d, ctypes.c_float(self.sm_scale),
-                _ptr(self.q_indptr), _ptr(self.q_offset), _ptr(self.kv_len), _ptr(self.ctx_indptr),
+                _ptr(self.q_indptr), _ptr(self.q_offset), _ptr(self.q_pos), _ptr(self.kv_len),
+                _ptr(self.ctx_indptr),
                 _ptr(self.q), _ptr(self.k_new), _ptr(self.v_new), _ptr(self.k_ctx), _ptr(self.v_ctx))
 
 
@@ -183,7 +188,7 @@ def expected_kv(wl, item: int) -> Tuple[np.ndarray, np.ndarray]:
     k = np.empty((L, call.hkv, call.d), np.uint16)
     v = np.empty_like(k)
     rc = lib().oracle_expected_kv(1, call.hkv, call.d, _ptr(call.q_indptr), _ptr(call.q_offset),
-                                  _ptr(call.kv_len), _ptr(call.ctx_indptr), _ptr(call.k_new),
+                                  _ptr(call.q_pos), _ptr(call.kv_len), _ptr(call.ctx_indptr), _ptr(call.k_new),
                                   _ptr(call.v_new), _ptr(call.k_ctx), _ptr(call.v_ctx), 0,
                                   _ptr(k), _ptr(v))
     if rc != 0:

@@ -33,7 +33,8 @@ def bf(x):
 # ------------------------------------------------------------ brute force
 def brute_force(wl):
     """Exact-rational scores, math.exp and math.fsum; assembles each item's
-    sequence on its own (fresh rows over [o, o+n), cache rows elsewhere)."""
+    sequence on its own (fresh row r at the row's position, cache rows
+    elsewhere)."""
     hq, hkv, d = wl.num_q_heads, wl.num_kv_heads, wl.head_dim
     G = hq // hkv
     sigma = Fraction(float(np.float32(wl.sm_scale)))
@@ -42,11 +43,12 @@ def brute_force(wl):
         q = wl.q(i).float().numpy()
         kn, vn = wl.k_new(i).float().numpy(), wl.v_new(i).float().numpy()
         kc, vc = wl.k_ctx(i), wl.v_ctx(i)
-        o, n, L = int(wl.q_offset[i]), wl.n(i), int(wl.kv_len[i])
+        n, L = wl.n(i), int(wl.kv_len[i])
+        row_at = {int(p): r for r, p in enumerate(wl.positions(i))}
         K, V = [], []
         for j in range(L):
-            if o <= j < o + n:
-                K.append(kn[j - o]); V.append(vn[j - o])
+            if j in row_at:
+                K.append(kn[row_at[j]]); V.append(vn[row_at[j]])
             else:
                 K.append(kc[j].float().numpy()); V.append(vc[j].float().numpy())
         out = np.zeros((n, hq, d))
@@ -65,6 +67,77 @@ def brute_force(wl):
         outs.append(out)
         lses.append(lse)
     return np.concatenate(outs), np.concatenate(lses)
+
+
+def brute_force_kv(wl, i):
+    """The item's cache after the call, assembled row by row on its own:
+    bf16 bits [L, Hkv, D] of K and V."""
+    row_at = {int(p): r for r, p in enumerate(wl.positions(i))}
+    kn, vn = wl.k_new(i), wl.v_new(i)
+    kc, vc = wl.k_ctx(i), wl.v_ctx(i)
+    K = torch.stack([kn[row_at[j]] if j in row_at else kc[j] for j in range(int(wl.kv_len[i]))])
+    V = torch.stack([vn[row_at[j]] if j in row_at else vc[j] for j in range(int(wl.kv_len[i]))])
+    bits = lambda t: t.contiguous().view(torch.int16).numpy().view(np.uint16)
+    return bits(K), bits(V)
+
+
+@pytest.mark.parametrize("hq,hkv", [(2, 2), (4, 2), (2, 1)])
+def test_brute_force_positions(hq, hkv):
+    # per-token cached decodes: scattered positions (first, last, adjacent,
+    # isolated) next to a block decode and a prefill
+    wl = workloads.make_workload("bfp", 8, hq=hq, hkv=hkv, d=8, decodes=[(2, 6)], prefills=[4],
+                                 pos_decodes=[([1, 4, 5], 8), ([0, 6], 7), ([3], 9), ([0, 1, 2, 3, 4], 5)])
+    out, lse = oracle.attention_all(wl)
+    ref_out, ref_lse = brute_force(wl)
+    assert np.abs(out - ref_out).max() <= 1e-14
+    assert np.abs(lse - ref_lse).max() <= 1e-14
+    for i in range(wl.num_items):
+        k, v = oracle.expected_kv(wl, i)
+        rk, rv = brute_force_kv(wl, i)
+        assert np.array_equal(k, rk) and np.array_equal(v, rv), f"item {i}"
+
+
+def test_contiguous_positions_equal_block_decode():
+    # a position list that is a contiguous range describes the block decode
+    blk = workloads.make_workload("blk", 4, hq=4, hkv=2, d=16, decodes=[(40, 100), (3, 35)], prefills=[])
+    pos = workloads.make_workload("pos", 4, hq=4, hkv=2, d=16, decodes=[], prefills=[],
+                                  pos_decodes=[(range(40, 72), 100), (range(3, 35), 35)])
+    a, la = oracle.attention_all(blk)
+    b, lb = oracle.attention_all(pos)
+    assert np.array_equal(a, b) and np.array_equal(la, lb)
+    for i in range(2):
+        ka, va = oracle.expected_kv(blk, i)
+        kb, vb = oracle.expected_kv(pos, i)
+        assert np.array_equal(ka, kb) and np.array_equal(va, vb)
+
+
+def test_refresh_with_cached_values_is_position_independent():
+    # fresh rows equal to the cached rows they replace leave the result that
+    # of the cache alone, whichever positions are refreshed; a wrong position
+    # map would mix in rows from other positions
+    L, n = 50, 6
+    wls = []
+    for k, pp in enumerate(([0, 7, 8, 30, 31, 49], [10, 11, 12, 13, 14, 15])):
+        wl = workloads.make_workload(f"same{k}", 2, hq=4, hkv=4, d=16, decodes=[], prefills=[],
+                                     pos_decodes=[(pp, L)])
+        ctx_k, ctx_v = wl.k_ctx(0).float(), wl.v_ctx(0).float()
+        q0 = workloads.make_workload("q", 2, hq=4, hkv=4, d=16, decodes=[], prefills=[],
+                                     pos_decodes=[([0, 7, 8, 30, 31, 49], L)]).q(0).float()
+        vals = {workloads.KIND_KNEW: ctx_k[pp].clone(), workloads.KIND_VNEW: ctx_v[pp].clone(),
+                workloads.KIND_Q: q0}
+        wl.value_fn = lambda item, kind, vals=vals: vals.get(kind)
+        wls.append(wl)
+    a, la = oracle.attention_all(wls[0])
+    b, lb = oracle.attention_all(wls[1])
+    assert np.array_equal(a, b) and np.array_equal(la, lb)
+    # and it is the attention over the cached sequence itself
+    K = wls[0].k_ctx(0).double().numpy()
+    V = wls[0].v_ctx(0).double().numpy()
+    q = wls[0].q(0).double().numpy()
+    s = np.einsum("rhd,jhd->rhj", q, K) * float(np.float32(wls[0].sm_scale))
+    w = np.exp(s - s.max(-1, keepdims=True))
+    ref = np.einsum("rhj,jhd->rhd", w / w.sum(-1, keepdims=True), V)
+    assert np.abs(a - ref).max() <= 1e-12
 
 
 @pytest.mark.parametrize("hq,hkv", [(2, 2), (4, 2), (2, 1)])

@@ -35,7 +35,7 @@ from __future__ import annotations
 
 import dataclasses
 import math
-from typing import Callable, List, Optional, Tuple
+from typing import Callable, List, Optional, Sequence, Tuple
 
 import numpy as np
 import torch
@@ -68,6 +68,10 @@ class Workload:
     # optional overrides: item -> callable(kind) -> fp32 tensor
     value_fn: Optional[Callable[[int, int], torch.Tensor]] = None
     page_size: int = PAGE_SIZE
+    # optional per-row positions, int32 [sum n]: row r of item i sits at
+    # q_pos[q_indptr[i] + r] instead of q_offset[i] + r (per-token cached
+    # decodes that recompute scattered positions)
+    q_pos: Optional[np.ndarray] = None
 
     @property
     def num_items(self) -> int:
@@ -79,6 +83,12 @@ class Workload:
 
     def n(self, i: int) -> int:
         return int(self.q_indptr[i + 1] - self.q_indptr[i])
+
+    def positions(self, i: int) -> np.ndarray:
+        """Sequence positions of item i's rows (int64 [n_i])."""
+        if self.q_pos is not None:
+            return self.q_pos[self.q_indptr[i]:self.q_indptr[i + 1]].astype(np.int64)
+        return np.arange(int(self.q_offset[i]), int(self.q_offset[i]) + self.n(i), dtype=np.int64)
 
     # ------------------------------------------------------------------ values
     def _draw(self, item: int, kind: int, shape: Tuple[int, ...], device="cpu") -> torch.Tensor:
@@ -233,22 +243,35 @@ def make_workload(name: str, seed: int, *, hq: int, hkv: int, d: int,
                   decodes: List[Tuple[int, int]], prefills: List[int],
                   rng: Optional[np.random.Generator] = None, pool_pages: Optional[int] = None,
                   q_scale: float = 1.0, page_size: int = PAGE_SIZE,
-                  sm_scale: Optional[float] = None) -> Workload:
+                  sm_scale: Optional[float] = None,
+                  pos_decodes: Sequence[Tuple[Sequence[int], int]] = ()) -> Workload:
     """decodes: list of (o, L) for 32-row block decodes (n = min(32, L - o));
+    pos_decodes: list of (positions, L) for decodes that recompute the given
+    strictly increasing positions (placed after the block decodes);
     prefills: list of L. Pages are drawn from ``rng`` (default: seeded by seed)."""
     if rng is None:
         rng = np.random.default_rng(seed)
-    q_off, kv_len, n_rows, pre = [], [], [], []
+    q_off, kv_len, n_rows, pre, pos = [], [], [], [], []
     for (o, L) in decodes:
         q_off.append(o)
         kv_len.append(L)
         n_rows.append(min(BLOCK, L - o))
         pre.append(False)
+        pos.append(np.arange(o, o + n_rows[-1]))
+    for (pp, L) in pos_decodes:
+        pp = np.asarray(pp, dtype=np.int64)
+        assert len(pp) >= 1 and (np.diff(pp) > 0).all() and pp[0] >= 0 and pp[-1] < L
+        q_off.append(int(pp[0]))
+        kv_len.append(L)
+        n_rows.append(len(pp))
+        pre.append(False)
+        pos.append(pp)
     for L in prefills:
         q_off.append(0)
         kv_len.append(L)
         n_rows.append(L)
         pre.append(True)
+        pos.append(np.arange(L))
     kv_len_a = np.asarray(kv_len, dtype=np.int32)
     npages = (kv_len_a.astype(np.int64) + page_size - 1) // page_size
     needed = int(npages.sum())
@@ -264,7 +287,8 @@ def make_workload(name: str, seed: int, *, hq: int, hkv: int, d: int,
                     q_indptr=q_indptr, q_offset=np.asarray(q_off, dtype=np.int32),
                     kv_len=kv_len_a, is_prefill=np.asarray(pre, dtype=bool),
                     page_indptr=page_indptr, page_ids=perm, num_pool_pages=pool,
-                    sm_scale=sm_scale, q_scale=q_scale, page_size=page_size)
+                    sm_scale=sm_scale, q_scale=q_scale, page_size=page_size,
+                    q_pos=np.concatenate(pos).astype(np.int32) if pos_decodes else None)
 
 
 def _decodes_from_prompts(rng, prompts, resp) -> List[Tuple[int, int]]:
