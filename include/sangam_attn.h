@@ -11,9 +11,13 @@
  *   at sequence positions o_i .. o_i+n_i-1 (the block-offset table) and a
  *   context of L_i positions. A block decode has n_i = 32 rows (one response
  *   block) and reuses the request's cached KV; a prefill has o_i = 0,
- *   n_i = L_i and brings its whole sequence. For each item the call
- *     1. writes the fresh rows k_new / v_new into the paged cache at positions
- *        [o_i, o_i+n_i), and
+ *   n_i = L_i and brings its whole sequence. A per-token cached decode
+ *   (Sec. 2.2, the dKV-Cache-PD variant: prompt KV fixed, response tokens
+ *   refreshed individually) recomputes up to 32 rows at arbitrary positions,
+ *   given by the optional position list q_pos instead of o_i. For each item
+ *   the call
+ *     1. writes the fresh rows k_new / v_new into the paged cache at the rows'
+ *        positions ([o_i, o_i+n_i), or the listed ones), and
  *     2. lets every query row attend, without a causal mask, to all positions
  *        [0, L_i) of the item's post-write sequence:
  *          out[r,h,:] = softmax_j(sm_scale * q[r,h,:] . K[j,g,:]) V[j,g,:]
@@ -24,7 +28,8 @@
  *
  * Layouts (row-major, contiguous, 16-byte aligned; bf16 = IEEE bfloat16 bits):
  *   q, out          [sum n_i, Hq, D]  bf16   (item i's rows start at q_indptr[i])
- *   k_new, v_new    [sum n_i, Hkv, D] bf16   (row t of item i = position o_i + t)
+ *   k_new, v_new    [sum n_i, Hkv, D] bf16   (row t of item i = position o_i + t, or the
+ *                                             t-th listed position)
  *   k_cache,v_cache [num_pool_pages, Hkv, page_size, D] bf16
  *                   position p of item i lives in page
  *                   page_ids[page_indptr[i] + p / page_size], slot p % page_size
@@ -78,6 +83,11 @@ typedef struct sangam_attn_desc {
     const int32_t *kv_len;      /* [num_items] L_i >= 1 */
     const int32_t *page_indptr; /* [num_items + 1], page_indptr[i+1]-page_indptr[i] = ceil(L_i/page_size) */
     const int32_t *page_ids;    /* [page_indptr[num_items]], in range, no page twice */
+    const int32_t *q_pos;       /* NULL, or [q_indptr[num_items]]: the sequence position of each
+                                   query row (row r of item i at q_pos[q_indptr[i] + r]); then
+                                   q_offset is ignored. Per item strictly increasing in [0, L_i).
+                                   An item whose positions are not one contiguous range (a
+                                   per-token cached decode) has n_i <= 32 and a cached context */
 } sangam_attn_desc;
 
 /*

@@ -56,6 +56,7 @@ class AttnDesc(ctypes.Structure):
         ("kv_len", ctypes.c_void_p),
         ("page_indptr", ctypes.c_void_p),
         ("page_ids", ctypes.c_void_p),
+        ("q_pos", ctypes.c_void_p),
     ]
 
 

@@ -52,8 +52,11 @@ class Plan:
 
 
 def make_desc(*, q_indptr, q_offset, kv_len, page_indptr, page_ids, num_q_heads, num_kv_heads,
-              head_dim, num_pool_pages, sm_scale, page_size=16, force_kv_splits=0, num_cus=0):
+              head_dim, num_pool_pages, sm_scale, page_size=16, force_kv_splits=0, num_cus=0,
+              q_pos=None):
     arrays = [_i32(x) for x in (q_indptr, q_offset, kv_len, page_indptr, page_ids)]
+    if q_pos is not None:
+        arrays.append(_i32(q_pos))
     d = AttnDesc()
     d.num_items = int(len(arrays[1]))
     d.num_q_heads = int(num_q_heads)
@@ -64,20 +67,22 @@ def make_desc(*, q_indptr, q_offset, kv_len, page_indptr, page_ids, num_q_heads,
     d.num_pool_pages = int(num_pool_pages)
     d.sm_scale = float(np.float32(sm_scale))
     d.num_cus = int(num_cus)
-    d.q_indptr, d.q_offset, d.kv_len, d.page_indptr, d.page_ids = (a.ctypes.data for a in arrays)
+    d.q_indptr, d.q_offset, d.kv_len, d.page_indptr, d.page_ids = (a.ctypes.data for a in arrays[:5])
+    d.q_pos = arrays[5].ctypes.data if q_pos is not None else None
     return d, arrays  # keep arrays alive while d is used
 
 
 def plan(*, q_indptr, q_offset, kv_len, page_indptr, page_ids, num_q_heads, num_kv_heads, head_dim,
-         num_pool_pages, sm_scale, page_size=16, force_kv_splits=0, num_cus=0,
+         num_pool_pages, sm_scale, page_size=16, force_kv_splits=0, num_cus=0, q_pos=None,
          device=None) -> Plan:
     """sangam_attn_plan: validate the batch and build its launch plan (host only).
-    With ``device`` the blob is also copied to that device."""
+    q_pos: optional per-row positions (per-token cached decodes). With
+    ``device`` the blob is also copied to that device."""
     d, keep = make_desc(q_indptr=q_indptr, q_offset=q_offset, kv_len=kv_len,
                         page_indptr=page_indptr, page_ids=page_ids, num_q_heads=num_q_heads,
                         num_kv_heads=num_kv_heads, head_dim=head_dim,
                         num_pool_pages=num_pool_pages, sm_scale=sm_scale, page_size=page_size,
-                        force_kv_splits=force_kv_splits, num_cus=num_cus)
+                        force_kv_splits=force_kv_splits, num_cus=num_cus, q_pos=q_pos)
     used = ctypes.c_size_t(0)
     st = lib.sangam_attn_plan(ctypes.byref(d), None, 0, ctypes.byref(used))
     if st not in (_lib.SANGAM_OK, -5):  # -5: buffer too small, *used holds the size

@@ -62,6 +62,8 @@ struct AttnArgs {
     uint16_t* out;
     float* lse;
     float* ws;
+    const int32_t* positions;    // rows of per-token cached decodes (kItemPosList items)
+    const uint32_t* page_info;   // per page of such items: listed slots and earlier rows
     int32_t hq;
     int32_t hkv;
     float scale_log2;
@@ -177,6 +179,8 @@ __global__ __launch_bounds__(64 * QW * KW, MINB) void attn_tiles_kernel(AttnArgs
 
     __shared__ __attribute__((aligned(1024))) uint8_t smem[2 * NSTAGE * TILE];
     __shared__ int32_t pages[MAX_PAGES];
+    __shared__ uint32_t pinfo[MAX_PAGES];  // page_info of the tile's pages (kItemPosList items)
+    __shared__ int32_t fpos[kWaveRows];    // the listed positions (kItemPosList items)
     __shared__ int32_t wpages[16];  // pages of the fresh rows this tile writes back
 
     const int tid = threadIdx.x;
@@ -202,11 +206,17 @@ __global__ __launch_bounds__(64 * QW * KW, MINB) void attn_tiles_kernel(AttnArgs
     const int nstages = (kv_end - kv_begin + STEP - 1) / STEP;
     // a whole prefill brings every position fresh: no page lookups
     const bool all_fresh = it.o == 0 && it.n == it.L;
+    // a per-token cached decode: its rows sit at listed positions
+    const bool plist = (it.flags & kItemPosList) != 0;
     const int pg0 = kv_begin >> 4;
     if (!all_fresh) {
         // the tile's page ids, once (the plan keeps such ranges <= kMaxCachedRange)
         const int npg = ((kv_end + 15) >> 4) - pg0;
-        for (int k = tid; k < npg; k += NT) pages[k] = a.page_ids[it.page_start + pg0 + k];
+        for (int k = tid; k < npg; k += NT) {
+            pages[k] = a.page_ids[it.page_start + pg0 + k];
+            if (plist) pinfo[k] = a.page_info[it.page_start + pg0 + k];
+        }
+        if (plist && tid < it.n) fpos[tid] = a.positions[it.pos_start + tid];
     }
 
     // ---- Q fragments (B operand: k = dims, n = query), zero for rows past n
@@ -273,10 +283,22 @@ __global__ __launch_bounds__(64 * QW * KW, MINB) void attn_tiles_kernel(AttnArgs
             if (tail) p = p < kv_end ? p : kv_begin;  // past the range: a valid row, masked later
             const int ck = (pos ^ swz_k<D>(r)) * 8;
             const int cv = (pos ^ swz_v<D>(r)) * 8;
+            // fresh row holding position p, counted from position o (row r
+            // sits at o + r in kfresh / vfresh), or -1 for a cached row
+            int fr;
+            if (all_fresh) {
+                fr = p;
+            } else if (plist) {
+                const uint32_t inf = pinfo[(p >> 4) - pg0];
+                const uint32_t below = inf & ((1u << (p & 15)) - 1u);
+                fr = (inf >> (p & 15)) & 1u ? int(inf >> kPageInfoRowShift) + __builtin_popcount(below) + it.o : -1;
+            } else {
+                fr = unsigned(p - it.o) < unsigned(it.n) ? p : -1;
+            }
             const uint16_t *ksrc, *vsrc;
-            if (all_fresh || unsigned(p - it.o) < unsigned(it.n)) {
-                ksrc = kfresh + (size_t)p * row_stride;
-                vsrc = vfresh + (size_t)p * row_stride;
+            if (fr >= 0) {
+                ksrc = kfresh + (size_t)fr * row_stride;
+                vsrc = vfresh + (size_t)fr * row_stride;
             } else {
                 const size_t off = (size_t)pages[(p >> 4) - pg0] * page_stride + (p & 15) * D;
                 ksrc = kcache + off;
@@ -301,8 +323,12 @@ __global__ __launch_bounds__(64 * QW * KW, MINB) void attn_tiles_kernel(AttnArgs
     // issues no global load whose wait would also drain the prefetch.
     const int group = a.hq / a.hkv;
     const bool wb_head = across ? t.q_head0 == t.kv_head * group : t.q_head0 % group == 0;
+    // positions written: [wb_lo, wb_hi) for a block; for a position list (a
+    // decode, so heads-across), its listed positions inside the span from the
+    // first to the last listed position
+    const int last_pos = plist ? a.positions[it.pos_start + it.n - 1] : it.o + it.n - 1;
     const int wb_lo = max(kv_begin, it.o + (across ? 0 : t.row0));
-    const int wb_hi = min(kv_end, it.o + (across ? it.n : min(it.n, t.row0 + 32 * QB * QW)));
+    const int wb_hi = min(kv_end, across ? last_pos + 1 : it.o + min(it.n, t.row0 + 32 * QB * QW));
     const bool writer = wb_head && wb_lo < wb_hi;
     const int wpg0 = wb_lo >> 4;
     auto write_back = [&](int st) {
@@ -311,6 +337,19 @@ __global__ __launch_bounds__(64 * QW * KW, MINB) void attn_tiles_kernel(AttnArgs
         if (lo >= hi) return;
         const uint8_t* kb = smem + (st % NSTAGE) * 2 * TILE;
         const uint8_t* vb = kb + TILE;
+        if (plist) {  // the listed positions inside [lo, hi); their pages are the tile's
+            for (int cidx = tid; cidx < it.n * NC; cidx += NT) {
+                const int p = fpos[cidx / NC], pos = cidx % NC;
+                if (p < lo || p >= hi) continue;
+                const int r = p - key0;
+                const u32x4 kv = *(const LDS u32x4*)(kb + r * ROWB + ((pos ^ swz_k<D>(r)) << 4));
+                const u32x4 vv = *(const LDS u32x4*)(vb + r * ROWB + ((pos ^ swz_v<D>(r)) << 4));
+                const size_t dst = (((size_t)pages[(p >> 4) - pg0] * a.hkv + t.kv_head) * 16 + (p & 15)) * D + pos * 8;
+                *(u32x4*)(a.k_cache + dst) = kv;
+                *(u32x4*)(a.v_cache + dst) = vv;
+            }
+            return;
+        }
         for (int cidx = tid; cidx < (hi - lo) * NC; cidx += NT) {
             const int p = lo + cidx / NC, pos = cidx % NC;
             const int r = p - key0;
@@ -473,7 +512,7 @@ __global__ __launch_bounds__(64 * QW * KW, MINB) void attn_tiles_kernel(AttnArgs
             asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     };
     for (int k = 0; k < NSTAGE - 1 && k < nstages; ++k) issue_stage(k, k);
-    if (writer && tid < ((wb_hi + 15) >> 4) - wpg0) wpages[tid] = a.page_ids[it.page_start + wpg0 + tid];
+    if (writer && !plist && tid < ((wb_hi + 15) >> 4) - wpg0) wpages[tid] = a.page_ids[it.page_start + wpg0 + tid];
     int st = 0;
     for (; st < full_stages; ++st) {
         wait_stage(st);
@@ -731,6 +770,8 @@ static sangam_status forward_impl(const void* plan_host, const void* plan_dev, c
                   static_cast<uint16_t*>(out),
                   lse,
                   static_cast<float*>(workspace),
+                  reinterpret_cast<const int32_t*>(pd + h->off_positions),
+                  reinterpret_cast<const uint32_t*>(pd + h->off_page_info),
                   h->hq,
                   h->hkv,
                   h->scale_log2};

@@ -117,18 +117,42 @@ extern "C" sangam_status sangam_attn_plan(const sangam_attn_desc* d, void* plan_
     const int G = hq / hkv;
     const int num_cus = d->num_cus ? d->num_cus : 256;
 
-    // ---- per-item validation
+    // ---- per-item validation. With a position list, an item whose rows sit
+    // on one contiguous range is a block (offset = its first position); any
+    // other is a per-token cached decode (kItemPosList).
     int64_t total_q = 0;
+    std::vector<int32_t> offset(n_items);
+    std::vector<char> listed(n_items, 0);
     for (int i = 0; i < n_items; ++i) {
         const int64_t n = int64_t(d->q_indptr[i + 1]) - d->q_indptr[i];
-        const int64_t o = d->q_offset[i], L = d->kv_len[i];
+        const int64_t L = d->kv_len[i];
         if (n < 1)
             return fail(SANGAM_ERR_INVALID_ARG, "item " + std::to_string(i) + ": n_i must be >= 1");
         if (L < 1)
             return fail(SANGAM_ERR_INVALID_ARG, "item " + std::to_string(i) + ": kv_len must be >= 1");
+        int64_t o = d->q_offset[i];
+        if (d->q_pos) {
+            const int32_t* pp = d->q_pos + d->q_indptr[i];
+            bool contiguous = true;
+            for (int64_t r = 0; r < n; ++r) {
+                if (pp[r] < 0 || pp[r] >= L || (r > 0 && pp[r] <= pp[r - 1]))
+                    return fail(SANGAM_ERR_INVALID_ARG, "item " + std::to_string(i) +
+                                                            ": positions must increase strictly inside [0, kv_len)");
+                contiguous = contiguous && pp[r] == pp[0] + r;
+            }
+            o = pp[0];
+            if (!contiguous) {
+                if (n > kWaveRows || n == L)
+                    return fail(SANGAM_ERR_INVALID_ARG,
+                                "item " + std::to_string(i) + ": a non-contiguous position list holds at most " +
+                                    std::to_string(kWaveRows) + " rows");
+                listed[i] = 1;
+            }
+        }
         if (o < 0 || o + n > L)
             return fail(SANGAM_ERR_INVALID_ARG,
                         "item " + std::to_string(i) + ": need 0 <= q_offset and q_offset + n <= kv_len");
+        offset[i] = int32_t(o);
         const int64_t np = int64_t(d->page_indptr[i + 1]) - d->page_indptr[i];
         if (np != ceil_div(L, d->page_size))
             return fail(SANGAM_ERR_INVALID_ARG,
@@ -187,15 +211,32 @@ extern "C" sangam_status sangam_attn_plan(const sangam_attn_desc* d, void* plan_
                               kForcedSplitLen);
 
     std::vector<ItemRec> items(n_items);
+    std::vector<int32_t> positions;    // rows of kItemPosList items
+    std::vector<uint32_t> page_info;   // per page, when any item is kItemPosList
+    if (std::find(listed.begin(), listed.end(), 1) != listed.end()) page_info.assign(total_pages, 0u);
     int64_t ws_floats = 0;
     int n_merge = 0, n_split_items = 0, max_splits = 1;
     for (int i = 0; i < n_items; ++i) {
         ItemRec& it = items[i];
         it.q_start = d->q_indptr[i];
         it.n = d->q_indptr[i + 1] - d->q_indptr[i];
-        it.o = d->q_offset[i];
+        it.o = offset[i];
         it.L = d->kv_len[i];
         it.page_start = d->page_indptr[i];
+        it.flags = listed[i] ? kItemPosList : 0;
+        it.pos_start = int32_t(positions.size());
+        if (listed[i]) {
+            const int32_t* pp = d->q_pos + it.q_start;
+            positions.insert(positions.end(), pp, pp + it.n);
+            for (int r = 0; r < it.n; ++r) page_info[it.page_start + (pp[r] >> 4)] |= 1u << (pp[r] & 15);
+            uint32_t before = 0;  // listed positions on earlier pages
+            for (int64_t k = 0; k < ceil_div(it.L, d->page_size); ++k) {
+                uint32_t& e = page_info[it.page_start + k];
+                const uint32_t cnt = uint32_t(__builtin_popcount(e));
+                e |= before << kPageInfoRowShift;
+                before += cnt;
+            }
+        }
         int64_t S;
         if (d->force_kv_splits > 0) {
             S = std::min<int64_t>(d->force_kv_splits, ceil_div(it.L, kKeyAlign));
@@ -296,6 +337,10 @@ extern "C" sangam_status sangam_attn_plan(const sangam_attn_desc* d, void* plan_
     off = align256(off + sizeof(TileRec) * pre.size());
     const uint64_t off_merge = off;
     off = align256(off + sizeof(MergeRow) * merge.size());
+    const uint64_t off_pos = off;
+    off = align256(off + sizeof(int32_t) * positions.size());
+    const uint64_t off_pinfo = off;
+    off = align256(off + sizeof(uint32_t) * page_info.size());
     const uint64_t total = off;
 
     *used = size_t(total);
@@ -335,11 +380,15 @@ extern "C" sangam_status sangam_attn_plan(const sangam_attn_desc* d, void* plan_
     h.off_decode_tiles = off_dec;
     h.off_prefill_tiles = off_pre;
     h.off_merge = off_merge;
+    h.off_positions = off_pos;
+    h.off_page_info = off_pinfo;
     std::memcpy(base, &h, sizeof h);
     if (!items.empty()) std::memcpy(base + off_items, items.data(), sizeof(ItemRec) * items.size());
     if (!dec.empty()) std::memcpy(base + off_dec, dec.data(), sizeof(TileRec) * dec.size());
     if (!pre.empty()) std::memcpy(base + off_pre, pre.data(), sizeof(TileRec) * pre.size());
     if (!merge.empty()) std::memcpy(base + off_merge, merge.data(), sizeof(MergeRow) * merge.size());
+    if (!positions.empty()) std::memcpy(base + off_pos, positions.data(), sizeof(int32_t) * positions.size());
+    if (!page_info.empty()) std::memcpy(base + off_pinfo, page_info.data(), sizeof(uint32_t) * page_info.size());
     return SANGAM_OK;
 }
 

@@ -9,7 +9,7 @@
 namespace sangam {
 
 constexpr uint32_t kPlanMagic = 0x50414753u;  // "SGAP"
-constexpr uint32_t kPlanVersion = 2;
+constexpr uint32_t kPlanVersion = 3;
 
 constexpr int kWaveRows = 32;       // query rows held by one wave (one decode block)
 constexpr int kPrefillQWaves = 4;   // waves of a prefill-shaped work-group
@@ -33,7 +33,19 @@ struct ItemRec {
     int32_t merge_base;  // first merge row of the item, -1 when not split
     int64_t ws_o;        // float offset of partial O  [num_splits][n][Hq][D]
     int64_t ws_lse;      // float offset of partial LSE [num_splits][n][Hq]
+    int32_t flags;       // kItemPosList or 0
+    int32_t pos_start;   // first entry of the item's positions (kItemPosList)
 };
+
+// ItemRec.flags: the rows sit at the listed positions (positions[pos_start +
+// r]), not at o + r; page_info[page_start + k] describes the item's page k.
+constexpr int32_t kItemPosList = 1;
+
+// page_info entry of a page of a kItemPosList item: bit s (s < 16) is set when
+// slot s holds a listed position; bits 16..31 count the listed positions on
+// the item's earlier pages, so the fresh row of slot s is that count plus the
+// set bits below s.
+constexpr int kPageInfoRowShift = 16;
 
 // TileRec.flags: the waves of a prefill-shaped work-group hold consecutive
 // query heads (q_head0 + wave, those inside the tile's GQA group) of one
@@ -100,11 +112,13 @@ struct PlanHeader {
     uint64_t off_decode_tiles;
     uint64_t off_prefill_tiles;
     uint64_t off_merge;
+    uint64_t off_positions;  // int32 positions of kItemPosList items
+    uint64_t off_page_info;  // uint32 per page (page_indptr order), when any item is kItemPosList
 };
 
-static_assert(sizeof(ItemRec) == 48, "ItemRec layout is part of the blob format");
+static_assert(sizeof(ItemRec) == 56, "ItemRec layout is part of the blob format");
 static_assert(sizeof(TileRec) == 32, "TileRec layout is part of the blob format");
 static_assert(sizeof(MergeRow) == 8, "MergeRow layout is part of the blob format");
-static_assert(sizeof(PlanHeader) == 160, "PlanHeader layout is part of the blob format");
+static_assert(sizeof(PlanHeader) == 176, "PlanHeader layout is part of the blob format");
 
 }  // namespace sangam

@@ -42,7 +42,7 @@ def run(wl, dev, force_splits=0, fill=float("nan"), want_lse=True):
                   page_indptr=wl.page_indptr, page_ids=wl.page_ids, num_q_heads=wl.num_q_heads,
                   num_kv_heads=wl.num_kv_heads, head_dim=wl.head_dim,
                   num_pool_pages=wl.num_pool_pages, sm_scale=wl.sm_scale,
-                  force_kv_splits=force_splits, device=dev)
+                  force_kv_splits=force_splits, q_pos=wl.q_pos, device=dev)
     out, lse = attn.forward(p, t["q"], t["k_new"], t["v_new"], t["k_cache"], t["v_cache"],
                             t["page_ids"], want_lse=want_lse)
     torch.cuda.synchronize()
@@ -231,6 +231,27 @@ def test_decode_sweep_points(dev, shape, batch):
     p, t, out, lse = run(wl, dev)
     check_full(wl, out, lse)
     check_cache(wl, t)
+
+
+@pytest.mark.parametrize("hq,hkv,d,prefills", [(8, 8, 64, ()), (32, 32, 128, ()), (28, 4, 128, ()),
+                                               (28, 4, 128, (150, 301)), (8, 2, 64, (97,))])
+@pytest.mark.parametrize("force", [0, 3])
+def test_token_cache_decodes(dev, hq, hkv, d, prefills, force):
+    """Per-token cached decodes: 32 rows at scattered response positions."""
+    wl = workloads.token_cache_decodes(4, hq=hq, hkv=hkv, d=d, count=6, prefills=prefills)
+    p, t, out, lse = run(wl, dev, force_splits=force)
+    check_full(wl, out, lse)
+    check_cache(wl, t)
+    check_pool_untouched(wl, t)
+
+
+def test_contiguous_list_is_the_block_decode(dev):
+    blk = workloads.make_workload("blk", 3, hq=28, hkv=4, d=128, decodes=[(300, 700), (64, 96)], prefills=[])
+    pos = workloads.make_workload("pos", 3, hq=28, hkv=4, d=128, decodes=[], prefills=[],
+                                  pos_decodes=[(range(300, 332), 700), (range(64, 96), 96)])
+    _, _, o1, l1 = run(blk, dev)
+    _, _, o2, l2 = run(pos, dev)
+    assert torch.equal(o1, o2) and torch.equal(l1, l2)
 
 
 def test_deterministic(dev):

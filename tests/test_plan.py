@@ -20,10 +20,12 @@ HEADER = np.dtype([
     ("num_split_items", "<i4"), ("max_splits", "<i4"), ("prefill_rows", "<i4"),
     ("n_fused_decode_tiles", "<i4"), ("reserved", "<i4"), ("workspace_bytes", "<i8"),
     ("off_items", "<u8"), ("off_decode_tiles", "<u8"), ("off_prefill_tiles", "<u8"), ("off_merge", "<u8"),
+    ("off_positions", "<u8"), ("off_page_info", "<u8"),
 ])
 ITEM = np.dtype([("q_start", "<i4"), ("n", "<i4"), ("o", "<i4"), ("L", "<i4"), ("page_start", "<i4"),
                  ("num_splits", "<i4"), ("split_len", "<i4"), ("merge_base", "<i4"),
-                 ("ws_o", "<i8"), ("ws_lse", "<i8")])
+                 ("ws_o", "<i8"), ("ws_lse", "<i8"), ("flags", "<i4"), ("pos_start", "<i4")])
+POS_LIST = 1
 TILE = np.dtype([("item", "<i4"), ("kv_head", "<i4"), ("q_head0", "<i4"), ("row0", "<i4"),
                  ("kv_begin", "<i4"), ("kv_end", "<i4"), ("split", "<i4"), ("flags", "<i4")])
 HEADS_ACROSS = 1
@@ -45,16 +47,16 @@ def plan_of(wl, **kw):
                      page_indptr=wl.page_indptr, page_ids=wl.page_ids,
                      num_q_heads=wl.num_q_heads, num_kv_heads=wl.num_kv_heads,
                      head_dim=wl.head_dim, num_pool_pages=wl.num_pool_pages,
-                     sm_scale=wl.sm_scale, **kw)
+                     sm_scale=wl.sm_scale, q_pos=wl.q_pos, **kw)
 
 
 def test_header_size_matches():
     # plan_format.h static_asserts the same sizes on the C side
     p = plan_of(workloads.tiny_mixed(0))
     h, *_ = parse(p)
-    assert h["magic"] == 0x50414753 and h["version"] == 2
+    assert h["magic"] == 0x50414753 and h["version"] == 3
     assert h["total_bytes"] == p.host.nbytes
-    assert HEADER.itemsize == 160 and ITEM.itemsize == 48 and TILE.itemsize == 32
+    assert HEADER.itemsize == 176 and ITEM.itemsize == 56 and TILE.itemsize == 32
 
 
 def coverage(wl, p):
@@ -102,6 +104,8 @@ def coverage(wl, p):
     lambda: workloads.make_workload("g7", 3, hq=28, hkv=4, d=128, decodes=[(0, 9000), (64, 300)],
                                     prefills=[200]),
     lambda: workloads.make_workload("g2", 4, hq=8, hkv=4, d=64, decodes=[(32, 700)], prefills=[100]),
+    lambda: workloads.token_cache_decodes(2, hq=8, hkv=8, d=64, count=5),
+    lambda: workloads.token_cache_decodes(3, hq=28, hkv=4, d=128, count=4, prefills=[150]),
 ])
 @pytest.mark.parametrize("force", [0, 1, 3, 8])
 def test_every_row_head_key_covered_once(mk, force):
@@ -322,3 +326,52 @@ def test_underfilled_decode_launch_splits_finer():
     # the same batch on a 16-CU part counts as full
     h, items, dec, pre, mer = parse(plan_of(workloads.decode_sweep("llada", 1), num_cus=16))
     assert (items["num_splits"] == 1).all()
+
+
+def test_position_list_items():
+    # per-token cached decodes: scattered lists become kItemPosList items with
+    # their positions and per-page slot masks in the blob; a contiguous list is
+    # a plain block at its first position
+    wl = workloads.make_workload("pl", 1, hq=4, hkv=2, d=64, decodes=[(40, 90)], prefills=[70],
+                                 pos_decodes=[([3, 17, 18, 40, 95], 100), (range(10, 42), 60),
+                                              ([0, 15, 16, 31, 32], 33)])
+    p = plan_of(wl)
+    h, items, dec, pre, mer = parse(p)
+    assert [int(f) for f in items["flags"]] == [0, POS_LIST, 0, POS_LIST, 0]
+    assert items["o"][2] == 10 and items["o"][1] == 3
+    pos = np.frombuffer(p.host, np.int32, count=10, offset=int(h["off_positions"]))
+    assert list(pos) == [3, 17, 18, 40, 95, 0, 15, 16, 31, 32]
+    assert items["pos_start"][1] == 0 and items["pos_start"][3] == 5
+    info = np.frombuffer(p.host, np.uint32, count=int(h["total_pages"]), offset=int(h["off_page_info"]))
+    for i in (1, 3):
+        listed = wl.positions(i)
+        pages = range(int(wl.page_indptr[i]), int(wl.page_indptr[i + 1]))
+        for k, e in enumerate(info[list(pages)]):
+            slots = [int(x) - 16 * k for x in listed if x // 16 == k]
+            assert int(e) & 0xFFFF == sum(1 << s_ for s_ in slots)
+            assert int(e) >> 16 == int(np.sum(listed < 16 * k))
+    # items without a list carry no page info
+    for i in (0, 2, 4):
+        assert not info[int(wl.page_indptr[i]):int(wl.page_indptr[i + 1])].any()
+
+
+@pytest.mark.parametrize("pos,L,msg", [
+    ([3, 3, 5], 10, "increase strictly"),
+    ([5, 4], 10, "increase strictly"),
+    ([2, 10], 10, "increase strictly"),
+    ([-1, 4], 10, "increase strictly"),
+    (list(range(0, 66, 2)), 70, "at most 32"),
+])
+def test_position_list_validation(pos, L, msg):
+    wl = workloads.make_workload("bad", 0, hq=2, hkv=2, d=64, decodes=[(0, 40)], prefills=[],
+                                 pos_decodes=[([1, 2, 7], 20)])
+    q_pos = np.concatenate([wl.q_pos, np.asarray(pos, np.int32)])
+    q_indptr = np.concatenate([wl.q_indptr, [wl.q_indptr[-1] + len(pos)]]).astype(np.int32)
+    kv_len = np.concatenate([wl.kv_len, [L]]).astype(np.int32)
+    npg = -(-L // 16)
+    page_indptr = np.concatenate([wl.page_indptr, [wl.page_indptr[-1] + npg]]).astype(np.int32)
+    page_ids = np.concatenate([wl.page_ids, np.arange(1000, 1000 + npg)]).astype(np.int32)
+    with pytest.raises(SangamError, match=msg):
+        attn.plan(q_indptr=q_indptr, q_offset=np.zeros(len(kv_len), np.int32), kv_len=kv_len,
+                  page_indptr=page_indptr, page_ids=page_ids, num_q_heads=2, num_kv_heads=2,
+                  head_dim=64, num_pool_pages=4096, sm_scale=0.125, q_pos=q_pos)

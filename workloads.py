@@ -378,6 +378,24 @@ CONFIGS = {
 }
 
 
+def token_cache_decodes(seed: int, *, hq: int, hkv: int, d: int, count: int, median: int = 500,
+                        sigma: float = 0.8, resp: int = 256, rows: int = 32,
+                        prefills: Sequence[int] = ()) -> Workload:
+    """Per-token cached decodes (the dKV-Cache-PD reading of Sec. 2.2): each of
+    `count` requests, prompt ~ LN(median, sigma) + `resp` response positions,
+    recomputes `rows` positions drawn without replacement from its response
+    (sorted) and reuses the cache everywhere else; optional whole prefills
+    join the batch."""
+    rng = np.random.default_rng(seed)
+    P = _lognormal_lengths(rng, count, median, sigma, 16, 4096)
+    pos = []
+    for p in P:
+        pp = np.sort(rng.choice(resp, size=rows, replace=False)) + int(p)
+        pos.append((pp, int(p) + resp))
+    return make_workload(f"token_cache_{hq}_{hkv}_{d}", seed, hq=hq, hkv=hkv, d=d, decodes=[],
+                         prefills=list(prefills), rng=rng, pos_decodes=pos)
+
+
 SWEEP_SHAPES = {"llada": (32, 32), "dream": (28, 4)}
 
 
