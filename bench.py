@@ -200,7 +200,8 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="dream_mixed",
-                    choices=["tiny_mixed", "llada_decode", "dream_mixed", "prefill_heavy", "long_decode"])
+                    choices=["tiny_mixed", "llada_decode", "dream_mixed", "prefill_heavy", "long_decode",
+                             "token_cache"])
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle work")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -240,7 +241,7 @@ def main():
     p = attn.plan(q_indptr=wl.q_indptr, q_offset=wl.q_offset, kv_len=wl.kv_len,
                   page_indptr=wl.page_indptr, page_ids=wl.page_ids, num_q_heads=wl.num_q_heads,
                   num_kv_heads=wl.num_kv_heads, head_dim=wl.head_dim,
-                  num_pool_pages=wl.num_pool_pages, sm_scale=wl.sm_scale)
+                  num_pool_pages=wl.num_pool_pages, sm_scale=wl.sm_scale, q_pos=wl.q_pos)
     plan_ms = (time.perf_counter() - t0) * 1e3
     p.to(dev)
     T, Hq, D = wl.total_q, wl.num_q_heads, wl.head_dim

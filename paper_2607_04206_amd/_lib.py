@@ -37,6 +37,7 @@ EXPORTS = (
     "sangam_attn_forward_timed",
     "sangam_last_error",
     "sangam_version",
+    "sangam_deficit_admit",
 )
 
 
@@ -98,6 +99,10 @@ def _load():
     lib.sangam_plan_item_splits.argtypes = [P, ctypes.c_int32, ctypes.POINTER(ctypes.c_int32), P,
                                             ctypes.c_int32]
     lib.sangam_plan_item_splits.restype = ctypes.c_int32
+    i64p = ctypes.POINTER(ctypes.c_int64)
+    lib.sangam_deficit_admit.argtypes = [ctypes.c_int64, ctypes.c_int64, ctypes.c_int32, P, ctypes.c_int32,
+                                         i64p, ctypes.POINTER(ctypes.c_int32)]
+    lib.sangam_deficit_admit.restype = ctypes.c_int32
     lib.sangam_attn_forward.argtypes = [P, P, P, P, P, P, P, P, P, P, P, S, P]
     lib.sangam_attn_forward.restype = ctypes.c_int32
     lib.sangam_attn_forward_timed.argtypes = [P, P, P, P, P, P, P, P, P, P, P, S, P, P]

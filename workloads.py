@@ -399,6 +399,13 @@ def token_cache_decodes(seed: int, *, hq: int, hkv: int, d: int, count: int, med
 SWEEP_SHAPES = {"llada": (32, 32), "dream": (28, 4)}
 
 
+def token_cache(seed: int = 0) -> Workload:
+    """LLaDA-8B-shaped per-token cached decodes: MHA 32/32, D 128; 32 requests
+    (prompts ~ LN(300, 0.8) in [16, 2048] + 256 response), each recomputing 32
+    scattered response positions over its whole cached context."""
+    return token_cache_decodes(seed, hq=32, hkv=32, d=128, count=32, median=300, sigma=0.8)
+
+
 def decode_sweep(shape: str, batch: int, seed: int = 0, L: int = 1024) -> Workload:
     """Decode-batch sweep point: `batch` block decodes of one model shape (LLaDA
     32/32 or Dream 28/4 heads, D 128), every request with L = 1024 cached
