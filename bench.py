@@ -194,6 +194,48 @@ def decode_sweep(args):
             del t, out, lse, ws
 
 
+def serve_trace(args):
+    """Serving loop over a synthetic trace (Dream 28/4 heads, D 128): per
+    iteration the deficit rule admits whole prefills next to the in-flight
+    block decodes, the host plans the batch and one attention call runs.
+    Prints one JSON line with per-iteration call times (HIP events) split by
+    iteration kind, admitted prefill tokens against tau, and prefill
+    queueing delays."""
+    import numpy as np
+    import torch
+
+    import workloads
+    from paper_2607_04206_amd.serve import ServingLoop
+
+    dev = torch.device("cuda:0")
+    reqs = workloads.serving_trace(args.seed, args.trace_iters, args.trace_rate)
+    loop = ServingLoop(reqs, hq=28, hkv=4, d=128, tau=args.tau, device=dev, seed=args.seed)
+    log = loop.run(args.trace_iters * 8)
+    torch.cuda.synchronize()
+    ms = np.asarray([r.events[0].elapsed_time(r.events[1]) for r in log])
+    mixed = np.asarray([r.prefills > 0 for r in log])
+    waits = [w for r in log for w in r.queue_waits]
+    def pct(x, q):
+        return float(np.percentile(x, q)) if len(x) else None
+    res = {
+        "trace": "serving_loop", "heads": "28/4", "head_dim": 128, "tau": args.tau,
+        "requests": len(reqs), "iterations": len(log), "rate_per_iteration": args.trace_rate,
+        "finished": sum(1 for s in loop.reqs if s.phase == "done"),
+        "mixed_iterations": int(mixed.sum()), "decode_only_iterations": int((~mixed).sum()),
+        "call_ms_mean": float(ms.mean()), "call_ms_p50": pct(ms, 50), "call_ms_p99": pct(ms, 99),
+        "decode_only_ms_mean": float(ms[~mixed].mean()) if (~mixed).any() else None,
+        "mixed_ms_mean": float(ms[mixed].mean()) if mixed.any() else None,
+        "mixed_ms_p99": pct(ms[mixed], 99),
+        "prefill_tokens_per_busy_iteration": float(np.mean([r.prefill_tokens for r in log])),
+        "prefill_tokens_max": int(max(r.prefill_tokens for r in log)),
+        "decodes_mean": float(np.mean([r.decodes for r in log])),
+        "prefill_wait_iterations_mean": float(np.mean(waits)) if waits else None,
+        "prefill_wait_iterations_p99": pct(waits, 99),
+        "plan_ms_mean": float(np.mean([r.plan_ms for r in log])),
+    }
+    print(json.dumps(res), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -211,6 +253,12 @@ def main():
     ap.add_argument("--decode-sweep", action="store_true",
                     help="instead of one workload: block-decode batches of 1..64 requests at L = 1024 "
                          "for the LLaDA (32/32) and Dream (28/4) head shapes, one JSON line each")
+    ap.add_argument("--serve-trace", action="store_true",
+                    help="instead of one workload: a serving loop over a synthetic request trace, each "
+                         "iteration's microbatch composed by the deficit token-budget rule (Dream 28/4 heads)")
+    ap.add_argument("--tau", type=int, default=4096, help="token budget per iteration (--serve-trace)")
+    ap.add_argument("--trace-iters", type=int, default=600, help="iterations (--serve-trace)")
+    ap.add_argument("--trace-rate", type=float, default=0.3, help="requests per iteration (--serve-trace)")
     ap.add_argument("--flush", action="store_true",
                     help="overwrite 512 MiB between steps (outside the timing) so no step reads "
                          "the previous one's data from the 256 MB Infinity Cache; steps are then "
@@ -223,6 +271,9 @@ def main():
         sys.exit(2)
     if args.decode_sweep:
         decode_sweep(args)
+        return
+    if args.serve_trace:
+        serve_trace(args)
         return
 
     import numpy as np

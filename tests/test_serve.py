@@ -1,0 +1,115 @@
+"""The serving loop (paper_2607_04206_amd/serve.py): requests cycle through
+whole prefills, block decodes and re-prefills at block boundaries (Sec. 2.2,
+Sec. 4.3) with each microbatch composed by the deficit rule (Alg. 1). The
+host-only runs plan every batch without a GPU; the GPU runs check one mixed
+iteration against the oracle."""
+import numpy as np
+import pytest
+import torch
+
+import workloads
+from oracle import oracle
+from paper_2607_04206_amd.serve import ServingLoop
+
+
+def host_run(seed, tau=2048, rate=0.4, iters=120):
+    reqs = workloads.serving_trace(seed, iters, rate, median=200)
+    loop = ServingLoop(reqs, hq=8, hkv=2, d=64, tau=tau, device=None)
+    return reqs, loop, loop.run(iters * 10)
+
+
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_request_lifecycle(seed):
+    reqs, loop, log = host_run(seed)
+    assert all(s.phase == "done" for s in loop.reqs) and loop.pool.free == loop.pool.num_pages
+    for r in reqs:
+        pre = [rec.t for rec in log for rid, kind in rec.batch if rid == r.rid and kind == "prefill"]
+        dec = [rec.t for rec in log for rid, kind in rec.batch if rid == r.rid and kind == "decode"]
+        # one whole prefill per block (the first, then a re-prefill at every
+        # block boundary), then the block's decodes in consecutive iterations:
+        # a seated decode is never displaced
+        assert len(pre) == len(r.steps) and len(dec) == sum(r.steps)
+        k = 0
+        for b, t0 in enumerate(pre):
+            assert dec[k:k + r.steps[b]] == list(range(t0 + 1, t0 + 1 + r.steps[b]))
+            k += r.steps[b]
+        assert pre[0] >= r.arrival
+
+
+@pytest.mark.parametrize("seed", [0, 1])
+def test_admission_respects_the_budget(seed):
+    tau = 2048
+    _, loop, log = host_run(seed, tau=tau)
+    carry = 0
+    for rec in log:
+        # prefill tokens fit the budget left by the decodes plus the carry,
+        # except the single prefill the idle rule admits into an empty batch
+        idle = rec.decodes == 0
+        if not (idle and rec.prefills == 1):
+            assert rec.prefill_tokens <= tau - 32 * rec.decodes + carry
+        carry = rec.deficit
+
+
+@pytest.mark.gpu
+def test_serving_loop_on_gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("needs a GPU")
+    dev = torch.device("cuda:0")
+    reqs = workloads.serving_trace(3, 40, 0.5, median=150)
+    loop = ServingLoop(reqs, hq=8, hkv=2, d=64, tau=1024, device=dev)
+    checked = 0
+    for t in range(400):
+        if not loop.busy():
+            break
+        rec = loop.step(t, timed=False, capture=checked == 0)
+        if rec is None:
+            continue
+        if rec.captured is not None:
+            if rec.decodes == 0 or rec.prefills == 0:
+                continue
+            c = rec.captured
+            print(f"[case] serving loop iteration {t}: {rec.decodes} decodes, {rec.prefills} prefills", flush=True)
+            check_iteration(c)
+            checked += 1
+    torch.cuda.synchronize()
+    assert checked == 1
+    assert all(s.phase == "done" for s in loop.reqs)
+    assert torch.isfinite(loop.out.float()).all()
+
+
+def check_iteration(c):
+    """One captured call against the oracle: the pre-call content of the
+    pages is the decodes' cached context."""
+    n_items = len(c["kv_len"])
+    nd = c["decodes"]
+    decodes = [(int(c["q_offset"][i]), int(c["kv_len"][i])) for i in range(nd)]
+    prefills = [int(c["kv_len"][i]) for i in range(nd, n_items)]
+    wl = workloads.make_workload("served", 0, hq=8, hkv=2, d=64, decodes=decodes, prefills=prefills)
+    qi = c["q_indptr"]
+    pi = c["page_indptr"]
+
+    def ctx(i, pages):
+        blk = pages[pi[i]:pi[i + 1]].cpu().float()  # [np, Hkv, 16, D]
+        return blk.permute(0, 2, 1, 3).reshape(-1, 2, 64)[:int(c["kv_len"][i])]
+
+    def value_fn(i, kind):
+        sl = slice(int(qi[i]), int(qi[i + 1]))
+        if kind == workloads.KIND_Q:
+            return c["q"][sl].cpu().float()
+        if kind == workloads.KIND_KNEW:
+            return c["k_new"][sl].cpu().float()
+        if kind == workloads.KIND_VNEW:
+            return c["v_new"][sl].cpu().float()
+        if kind == workloads.KIND_KCTX:
+            return ctx(i, c["k_pages"])
+        if kind == workloads.KIND_VCTX:
+            return ctx(i, c["v_pages"])
+        return None
+
+    wl.value_fn = value_fn
+    wl.sm_scale = c["sm_scale"]
+    ref, ref_lse = oracle.attention_all(wl)
+    got = c["out"].float().cpu().numpy()
+    d = np.abs(got - ref)
+    assert d.max() <= 1e-2 and d.mean() <= 1e-3, (d.max(), d.mean())
+    assert np.abs(c["lse"].cpu().numpy() - ref_lse).max() <= 4e-3

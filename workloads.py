@@ -396,6 +396,34 @@ def token_cache_decodes(seed: int, *, hq: int, hkv: int, d: int, count: int, med
                          prefills=list(prefills), rng=rng, pos_decodes=pos)
 
 
+@dataclasses.dataclass
+class TraceRequest:
+    """One request of a synthetic serving trace."""
+    rid: int
+    arrival: int             # iteration at which it arrives
+    prompt: int              # prompt tokens P
+    resp: int                # appended masked response tokens R (R / 32 blocks)
+    steps: List[int]         # denoising steps of each block (block decodes per block)
+
+
+def serving_trace(seed: int, iterations: int, rate: float, *, median: int = 500, sigma: float = 0.8,
+                  resp: int = 256, min_steps: int = 2, max_steps: int = 8) -> List[TraceRequest]:
+    """Synthetic request stream for a serving loop (stands in for the paper's
+    traces, Sec. 6.1): Poisson arrivals at `rate` requests per iteration,
+    prompts ~ LN(median, sigma) in [16, 4096], `resp` appended masks in blocks
+    of 32, and per block a number of denoising steps (block decodes) drawn
+    uniformly from [min_steps, max_steps] (the confidence-threshold sampler
+    unmasks a variable number of tokens per step, Sec. 3.2)."""
+    rng = np.random.default_rng(seed)
+    reqs: List[TraceRequest] = []
+    for t in range(iterations):
+        for _ in range(int(rng.poisson(rate))):
+            P = int(_lognormal_lengths(rng, 1, median, sigma, 16, 4096)[0])
+            steps = [int(x) for x in rng.integers(min_steps, max_steps + 1, size=resp // BLOCK)]
+            reqs.append(TraceRequest(len(reqs), t, P, resp, steps))
+    return reqs
+
+
 SWEEP_SHAPES = {"llada": (32, 32), "dream": (28, 4)}
 
 
