@@ -254,6 +254,33 @@ __global__ __launch_bounds__(64 * QW * KW, MINB) void attn_tiles_kernel(AttnArgs
         foff_k[j] = uint32_t(r * row_stride * 2 + ((pos ^ swz_k<D>(r)) << 4));
         foff_v[j] = uint32_t(r * row_stride * 2 + ((pos ^ swz_v<D>(r)) << 4));
     }
+    // the same within a 16-row page (K/V head chunk of the cache) for a stage
+    // that starts on a page boundary: key row r_j sits in slot r_j mod 16 of
+    // the stage's page r_j / 16
+    uint32_t poff_k[NJ], poff_v[NJ];
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) {
+        const int P = j * NT + tid;
+        const int r = P / NC;
+        const int pos = P % NC;
+        poff_k[j] = uint32_t((r & 15) * ROWB + ((pos ^ swz_k<D>(r)) << 4));
+        poff_v[j] = uint32_t((r & 15) * ROWB + ((pos ^ swz_v<D>(r)) << 4));
+    }
+    // A full stage with no fresh row reads only cached rows. When it starts
+    // on a page boundary, each wave's copy instruction covers 64 / NC key rows
+    // of one page, so the page base is wave-uniform (scalar registers) and
+    // the lanes add the precomputed offsets: no per-lane page lookup,
+    // freshness test or 64-bit address arithmetic on the common path.
+    auto stage_all_cached = [&](int key0) -> bool {
+        if (all_fresh || (kv_begin & 15) != 0) return false;
+        if (plist) {
+            uint32_t slots = 0;
+#pragma unroll
+            for (int k = 0; k < STEP / 16; ++k) slots |= pinfo[(key0 >> 4) - pg0 + k];
+            return (uniform(int(slots & 0xFFFFu))) == 0;
+        }
+        return key0 + STEP <= it.o || key0 >= it.o + it.n;
+    };
 
     auto issue_stage = [&](int st, int buf) {
         uint8_t* kb = smem + buf * 2 * TILE;
@@ -270,6 +297,25 @@ __global__ __launch_bounds__(64 * QW * KW, MINB) void attn_tiles_kernel(AttnArgs
                 const int dst = (j * NT + wave * 64) * 16;
                 lds_copy16(kbase, foff_k[j], (LDS void*)(kb + dst));
                 lds_copy16(vbase, foff_v[j], (LDS void*)(vb + dst));
+            }
+            return;
+        }
+        if (!tail && stage_all_cached(key0)) {
+            const int prel = (key0 >> 4) - pg0;  // the stage's first page among the tile's
+            int pid[NJ];
+#pragma unroll
+            for (int j = 0; j < NJ; ++j) {
+                pid[j] = 0;
+                if ((NCH % NT) == 0 || j * NT + wave * 64 < NCH)
+                    pid[j] = pages[prel + (((j * NT + wave * 64) / NC) >> 4)];
+            }
+#pragma unroll
+            for (int j = 0; j < NJ; ++j) {
+                if ((NCH % NT) != 0 && j * NT + wave * 64 >= NCH) break;  // wave-uniform
+                const size_t off = (size_t)uniform(pid[j]) * page_stride;
+                const int dst = (j * NT + wave * 64) * 16;
+                lds_copy16(kcache + off, poff_k[j], (LDS void*)(kb + dst));
+                lds_copy16(vcache + off, poff_v[j], (LDS void*)(vb + dst));
             }
             return;
         }

@@ -57,13 +57,16 @@ def test_serving_loop_on_gpu():
     dev = torch.device("cuda:0")
     reqs = workloads.serving_trace(3, 40, 0.5, median=150)
     loop = ServingLoop(reqs, hq=8, hkv=2, d=64, tau=1024, device=dev)
+    loop.out.fill_(float("nan"))  # rows no call wrote stay NaN
     checked = 0
+    rows_written = 0
     for t in range(400):
         if not loop.busy():
             break
         rec = loop.step(t, timed=False, capture=checked == 0)
         if rec is None:
             continue
+        rows_written = max(rows_written, 32 * rec.decodes + rec.prefill_tokens)
         if rec.captured is not None:
             if rec.decodes == 0 or rec.prefills == 0:
                 continue
@@ -74,7 +77,9 @@ def test_serving_loop_on_gpu():
     torch.cuda.synchronize()
     assert checked == 1
     assert all(s.phase == "done" for s in loop.reqs)
-    assert torch.isfinite(loop.out.float()).all()
+    # every row some call wrote holds a finite output
+    assert rows_written > 0
+    assert torch.isfinite(loop.out[:rows_written].float()).all()
 
 
 def check_iteration(c):
