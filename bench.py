@@ -236,6 +236,66 @@ def serve_trace(args):
     print(json.dumps(res), flush=True)
 
 
+def kv_transfer(args):
+    """Paged-KV export and import (the hand-off of requests' KV between workers
+    in the hybrid configuration) over the cached contexts of the LLaDA decode
+    batch (32 requests, 32 KV heads), the Dream mixed batch (50 requests, 4 KV
+    heads) and the long decode batch (256 requests, 32 KV heads). Each copy is
+    one launch; times are HIP events around it on the launch stream. Bytes
+    moved = every position's K and V read once and written once."""
+    import numpy as np
+    import torch
+
+    import workloads
+    from paper_2607_04206_amd import kv
+
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream(dev)
+    for name in ("llada_decode", "dream_mixed", "long_decode"):
+        wl = getattr(workloads, name)(args.seed)
+        hkv, d = wl.num_kv_heads, wl.head_dim
+        rng = np.random.default_rng(args.seed)
+        counts = (wl.kv_len.astype(np.int64) + 15) // 16
+        indptr = np.zeros(len(counts) + 1, np.int32)
+        indptr[1:] = np.cumsum(counts)
+        pool = int(indptr[-1]) * 2
+        src = rng.permutation(pool)[:indptr[-1]].astype(np.int32)
+        dst = rng.permutation(pool)[:indptr[-1]].astype(np.int32)
+        ps = kv.plan(kv_len=wl.kv_len, page_indptr=indptr, page_ids=src, num_kv_heads=hkv, head_dim=d,
+                     num_pool_pages=pool, device=dev)
+        pd = kv.plan(kv_len=wl.kv_len, page_indptr=indptr, page_ids=dst, num_kv_heads=hkv, head_dim=d,
+                     num_pool_pages=pool, device=dev)
+        shape = (pool, hkv, 16, d)
+        ka = torch.randn(shape, device=dev).to(torch.bfloat16)
+        va = torch.randn(shape, device=dev).to(torch.bfloat16)
+        kb, vb = torch.empty_like(ka), torch.empty_like(va)
+        pk = torch.empty((ps.rows, hkv, d), dtype=torch.bfloat16, device=dev)
+        pv = torch.empty_like(pk)
+        res = {"bench": "kv_transfer", "batch": name, "requests": int(wl.num_items), "kv_heads": hkv,
+               "head_dim": d, "positions": ps.rows}
+        moved = 2 * 2 * ps.rows * hkv * d * 2  # K and V, read and written
+        for op, call in (("export", lambda: kv.kv_export(ps, ka, va, pk, pv)),
+                         ("import", lambda: kv.kv_import(pd, pk, pv, kb, vb))):
+            for _ in range(args.warmup):
+                call()
+            evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+                   for _ in range(args.steps)]
+            torch.cuda.synchronize()
+            for a, b in evs:
+                a.record(stream)
+                call()
+                b.record(stream)
+            torch.cuda.synchronize()
+            us = float(np.mean([a.elapsed_time(b) for a, b in evs])) * 1e3
+            res[f"{op}_us"] = us
+            res[f"{op}_gbs"] = moved / (us / 1e6) / 1e9
+            res[f"{op}_hbm_frac"] = res[f"{op}_gbs"] / PEAK_HBM_GBS
+        res["bytes_moved_per_copy"] = moved
+        print(json.dumps(res), flush=True)
+        del ka, va, kb, vb, pk, pv
+        torch.cuda.empty_cache()
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -259,6 +319,8 @@ def main():
     ap.add_argument("--tau", type=int, default=4096, help="token budget per iteration (--serve-trace)")
     ap.add_argument("--trace-iters", type=int, default=600, help="iterations (--serve-trace)")
     ap.add_argument("--trace-rate", type=float, default=0.3, help="requests per iteration (--serve-trace)")
+    ap.add_argument("--kv-transfer", action="store_true",
+                    help="time the paged-KV export / import of three batches' cached contexts")
     ap.add_argument("--flush", action="store_true",
                     help="overwrite 512 MiB between steps (outside the timing) so no step reads "
                          "the previous one's data from the 256 MB Infinity Cache; steps are then "
@@ -274,6 +336,9 @@ def main():
         return
     if args.serve_trace:
         serve_trace(args)
+        return
+    if args.kv_transfer:
+        kv_transfer(args)
         return
 
     import numpy as np

@@ -1,4 +1,5 @@
-"""ctypes declarations of the C ABI in include/sangam_attn.h.
+"""ctypes declarations of the C ABI in include/sangam_attn.h, sangam_sched.h
+and sangam_kv.h.
 
 Loads the in-tree ``libsangam_attn.so``; there is no fallback: if the
 library is missing or does not load, importing this module raises.
@@ -38,6 +39,10 @@ EXPORTS = (
     "sangam_last_error",
     "sangam_version",
     "sangam_deficit_admit",
+    "sangam_kv_plan",
+    "sangam_kv_plan_rows",
+    "sangam_kv_export",
+    "sangam_kv_import",
 )
 
 
@@ -58,6 +63,19 @@ class AttnDesc(ctypes.Structure):
         ("page_indptr", ctypes.c_void_p),
         ("page_ids", ctypes.c_void_p),
         ("q_pos", ctypes.c_void_p),
+    ]
+
+
+class KvDesc(ctypes.Structure):
+    _fields_ = [
+        ("num_items", ctypes.c_int32),
+        ("num_kv_heads", ctypes.c_int32),
+        ("head_dim", ctypes.c_int32),
+        ("page_size", ctypes.c_int32),
+        ("num_pool_pages", ctypes.c_int64),
+        ("kv_len", ctypes.c_void_p),
+        ("page_indptr", ctypes.c_void_p),
+        ("page_ids", ctypes.c_void_p),
     ]
 
 
@@ -107,6 +125,14 @@ def _load():
     lib.sangam_attn_forward.restype = ctypes.c_int32
     lib.sangam_attn_forward_timed.argtypes = [P, P, P, P, P, P, P, P, P, P, P, S, P, P]
     lib.sangam_attn_forward_timed.restype = ctypes.c_int32
+    lib.sangam_kv_plan.argtypes = [ctypes.POINTER(KvDesc), P, S, ctypes.POINTER(S)]
+    lib.sangam_kv_plan.restype = ctypes.c_int32
+    lib.sangam_kv_plan_rows.argtypes = [P]
+    lib.sangam_kv_plan_rows.restype = ctypes.c_int64
+    lib.sangam_kv_export.argtypes = [P, P, P, P, P, P, P]
+    lib.sangam_kv_export.restype = ctypes.c_int32
+    lib.sangam_kv_import.argtypes = [P, P, P, P, P, P, P]
+    lib.sangam_kv_import.restype = ctypes.c_int32
     lib.sangam_last_error.argtypes = []
     lib.sangam_last_error.restype = ctypes.c_char_p
     lib.sangam_version.argtypes = []

@@ -487,3 +487,46 @@ def gather_item_cache(wl: Workload, pool: torch.Tensor, i: int) -> torch.Tensor:
     pages = torch.from_numpy(wl.item_pages(i).astype(np.int64)).to(pool.device)
     blk = pool[pages].permute(0, 2, 1, 3).reshape(-1, wl.num_kv_heads, wl.head_dim)
     return blk[:int(wl.kv_len[i])]
+
+
+@dataclasses.dataclass
+class KvTransferCase:
+    """A batch of requests to move between two paged pools: the source page
+    table (sender's pool) and an unrelated destination page table (receiver's
+    pool), with the source pool's contents as bf16 bit patterns."""
+    name: str
+    kv_len: np.ndarray       # [n] int32
+    page_indptr: np.ndarray  # [n + 1] int32
+    src_pages: np.ndarray    # [total pages] int32, pages of the source pool
+    dst_pages: np.ndarray    # [total pages] int32, pages of the destination pool
+    num_pool_pages: int
+    num_kv_heads: int
+    head_dim: int
+    pool_k: np.ndarray       # [num_pool_pages, Hkv, 16, D] uint16
+    pool_v: np.ndarray
+
+    @property
+    def rows(self) -> int:
+        return int(self.kv_len.sum())
+
+
+def kv_transfer_case(name: str, seed: int, kv_len: Sequence[int], *, hkv: int, d: int,
+                     spare_pages: int = 3) -> KvTransferCase:
+    """Requests of the given lengths laid out on random pages of a pool with
+    `spare_pages` unused pages per used one; both page tables are drawn
+    without replacement from the same pool size. Pool values: standard normal
+    draws rounded to bf16 (every slot, listed or not)."""
+    rng = np.random.default_rng(seed)
+    kv_len = np.asarray(kv_len, np.int32)
+    counts = (kv_len.astype(np.int64) + 15) // 16
+    page_indptr = np.zeros(len(kv_len) + 1, np.int32)
+    page_indptr[1:] = np.cumsum(counts)
+    total = int(page_indptr[-1])
+    pool = max(total * (1 + spare_pages), 1)
+    src = rng.permutation(pool)[:total].astype(np.int32)
+    dst = rng.permutation(pool)[:total].astype(np.int32)
+    g = torch.Generator(device="cpu").manual_seed(seed)
+    shape = (pool, hkv, 16, d)
+    pk = torch.randn(shape, generator=g).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    pv = torch.randn(shape, generator=g).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    return KvTransferCase(name, kv_len, page_indptr, src, dst, pool, hkv, d, pk, pv)
