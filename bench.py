@@ -322,9 +322,10 @@ def main():
     ap.add_argument("--kv-transfer", action="store_true",
                     help="time the paged-KV export / import of three batches' cached contexts")
     ap.add_argument("--flush", action="store_true",
-                    help="overwrite 512 MiB between steps (outside the timing) so no step reads "
-                         "the previous one's data from the 256 MB Infinity Cache; steps are then "
-                         "timed by events")
+                    help="read 1 GiB of other data between steps (outside the timing) so no step "
+                         "reads the previous one's data from the 256 MB Infinity Cache; steps are "
+                         "then timed by events. A read, not a write: written lines would be "
+                         "written back to HBM during the next step")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -381,7 +382,7 @@ def main():
         arr = (ctypes.c_void_p * 6)(*[e.cuda_event if e is not None else None for e in evs])
         return evs, arr
 
-    flush_buf = torch.empty((512 << 20,), dtype=torch.uint8, device=dev) if args.flush else None
+    flush_buf = torch.ones((1 << 28,), dtype=torch.float32, device=dev) if args.flush else None
     if args.copy_calib_mib > 0:
         src = torch.ones((args.copy_calib_mib << 20,), dtype=torch.uint8, device=dev)
         dst = torch.empty_like(src)
@@ -402,7 +403,7 @@ def main():
     torch.cuda.synchronize()
     for k in range(n_phase):
         if args.flush:
-            flush_buf.fill_(k & 0xFF)
+            flush_buf.sum()
         check(lib.sangam_attn_forward_timed(*args_c, evsets[k][1]))
     torch.cuda.synchronize()
     phase_ms = {}
@@ -420,7 +421,7 @@ def main():
         step_ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
                    for _ in range(K)]
         for k in range(K):
-            flush_buf.fill_(k & 0xFF)
+            flush_buf.sum()
             step_ev[k][0].record(stream)
             check(lib.sangam_attn_forward_timed(*args_c, evsets[k][1]))
             step_ev[k][1].record(stream)
