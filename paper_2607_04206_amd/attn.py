@@ -28,6 +28,8 @@ class Plan:
     num_kv_heads: int
     head_dim: int
     total_q: int
+    num_pool_pages: int = 0  # pool size the plan's page ids were checked against
+    total_pages: int = 0     # entries of page_ids the kernels read
 
     @property
     def workspace_bytes(self) -> int:
@@ -94,7 +96,8 @@ def plan(*, q_indptr, q_offset, kv_len, page_indptr, page_ids, num_q_heads, num_
     del keep
     p = Plan(host=buf, dev=None, info=info, num_q_heads=int(num_q_heads),
              num_kv_heads=int(num_kv_heads), head_dim=int(head_dim),
-             total_q=int(info.total_q_rows))
+             total_q=int(info.total_q_rows), num_pool_pages=int(num_pool_pages),
+             total_pages=int(_i32(page_indptr)[-1]))
     if device is not None:
         p.to(device)
     return p
@@ -131,7 +134,12 @@ def forward(p: Plan, q: torch.Tensor, k_new: torch.Tensor, v_new: torch.Tensor,
     _need(v_cache, "v_cache", torch.bfloat16, tuple(k_cache.shape), dev)
     if k_cache.dim() != 4 or k_cache.shape[1] != Hkv or k_cache.shape[2] != 16 or k_cache.shape[3] != D:
         raise ValueError("k_cache must be [num_pool_pages, Hkv, 16, D]")
+    if k_cache.shape[0] < p.num_pool_pages:
+        raise ValueError(f"the plan addresses {p.num_pool_pages} pool pages, k_cache holds {k_cache.shape[0]}")
     _need(page_ids, "page_ids", torch.int32, None, dev)
+    if page_ids.dim() != 1 or page_ids.numel() < p.total_pages:
+        raise ValueError(f"page_ids must be a 1-D tensor of at least {p.total_pages} entries "
+                         "(the plan's page table, on the device)")
     if p.dev is None or p.dev.device != dev:
         p.to(dev)
     if out is None:

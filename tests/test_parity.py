@@ -261,6 +261,40 @@ def test_deterministic(dev):
     assert torch.equal(o1, o2) and torch.equal(l1, l2)
 
 
+def test_graph_capture_replays(dev):
+    """The forward is only kernel launches on the caller's stream, so a HIP
+    graph can hold it: every replay (with eager work on the same buffers in
+    between) reproduces the eager call's bits, the split merge included."""
+    from paper_2607_04206_amd import attn
+    wl = workloads.ragged_small(2, hq=8, hkv=2, d=128)
+    p, t, out0, lse0 = run(wl, dev, force_splits=2)
+    assert p.workspace_bytes > 0
+    check_full(wl, out0, lse0)
+    out = torch.empty_like(out0)
+    lse = torch.empty_like(lse0)
+    ws = torch.empty((p.workspace_bytes,), dtype=torch.uint8, device=dev)
+    args = (p, t["q"], t["k_new"], t["v_new"], t["k_cache"], t["v_cache"], t["page_ids"])
+    side = torch.cuda.Stream(dev)
+    side.wait_stream(torch.cuda.current_stream(dev))
+    with torch.cuda.stream(side):
+        attn.forward(*args, out=out, lse=lse, workspace=ws)
+    torch.cuda.current_stream(dev).wait_stream(side)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        attn.forward(*args, out=out, lse=lse, workspace=ws)
+    for r in range(3):
+        out.fill_(float("nan"))
+        lse.fill_(float("nan"))
+        ws.zero_()
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(out.view(torch.int16), out0.view(torch.int16)), f"replay {r}: out differs"
+        assert torch.equal(lse, lse0), f"replay {r}: lse differs"
+    check_cache(wl, t)
+
+
 # --------------------------------------------------------------- invariants
 def test_constant_v_and_equal_keys(dev):
     L, o = 700, 333
