@@ -182,7 +182,10 @@ def decode_sweep(args):
             torch.cuda.synchronize()
             launches = np.mean([[e[2 * j].elapsed_time(e[2 * j + 1]) for j in range(3)] for e, _ in evs], 0)
             F, Bytes = wl.flops(), wl.hbm_bytes()
-            kern = float(launches[1])  # the decode-shaped launch (no prefill in the batch)
+            # the launch that holds the block decodes: prefill-shaped heads-across
+            # tiles for a small GQA batch, else the decode-shaped launch
+            fused = int(p.info.num_fused_decode_tiles) > 0
+            kern = float(launches[0] if fused else launches[1])
             print(json.dumps({
                 "sweep": "decode_batch", "shape": shape, "num_q_heads": wl.num_q_heads,
                 "num_kv_heads": wl.num_kv_heads, "batch": B, "kv_len": 1024, "ms_per_call": ms,
@@ -190,7 +193,9 @@ def decode_sweep(args):
                 "tflops": F / (ms / 1e3) / 1e12, "hbm_gbs": Bytes / (ms / 1e3) / 1e9,
                 "kernel_hbm_frac": Bytes / (kern / 1e3) / (PEAK_HBM_GBS * 1e9),
                 "kernel_mfma_frac": F / (kern / 1e3) / (PEAK_BF16_TFLOPS * 1e12),
-                "splits": int(p.info.num_split_items), "tiles": int(p.info.num_decode_tiles)}), flush=True)
+                "decode_launch": "prefill-shaped (heads across)" if fused else "decode-shaped",
+                "splits": int(p.info.num_split_items),
+                "tiles": int(p.info.num_prefill_tiles if fused else p.info.num_decode_tiles)}), flush=True)
             del t, out, lse, ws
 
 

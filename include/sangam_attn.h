@@ -116,9 +116,11 @@ typedef struct sangam_plan_info {
     int32_t decode_q_waves;    /* waves per decode work-group that hold query rows */
     int32_t decode_kv_waves;   /* waves per decode work-group that split the context */
     int32_t num_fused_decode_tiles; /* prefill-shaped work-groups that hold block decodes:
-                                       in a batch with prefills, a GQA group of >= 4 query
+                                       in a batch with prefills, or a decode-only batch too
+                                       small to fill the CUs, a GQA group of >= 4 query
                                        heads per KV head puts its block decodes there (one
-                                       query head per wave), unsplit up to 8192 keys */
+                                       query head per wave); with prefills unsplit up to
+                                       8192 keys */
     int64_t total_q_rows;      /* sum n_i */
     int64_t workspace_bytes;
     int64_t plan_bytes;

@@ -444,8 +444,12 @@ __global__ __launch_bounds__(64 * QW * KW, MINB) void attn_tiles_kernel(AttnArgs
 
     // S^T = K Q^T for this wave's NB 32-key blocks of stage st: rows = keys,
     // columns = queries; each K fragment feeds the QB query blocks
+    // The QK^T MFMAs run at raised wave priority: with two waves per SIMD,
+    // the wave that reaches its QK^T chain keeps the matrix core fed while the
+    // other works through its softmax (measured about 1 % faster on prefills).
     auto qk = [&](int st, f32x16 (&s)[QB][NB]) {
         const uint8_t* kb = smem + (st % NSTAGE) * 2 * TILE + ks * KT * ROWB;
+        __builtin_amdgcn_s_setprio(1);
 #pragma unroll
         for (int b = 0; b < NB; ++b) {
 #pragma unroll
@@ -460,6 +464,7 @@ __global__ __launch_bounds__(64 * QW * KW, MINB) void attn_tiles_kernel(AttnArgs
                     s[qb][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[qb][k], s[qb][b], 0, 0, 0);
             }
         }
+        __builtin_amdgcn_s_setprio(0);
     };
 
     // Online softmax of stage st's scores (exp2 domain) and O^T += V^T P^T.

@@ -94,10 +94,11 @@ struct PlanHeader {
     int32_t decode_kw;
     int32_t decode_nb;   // 32-key blocks per wave per stage
     // prefill-shaped launch: items with n > kWaveRows; kPrefillQWaves waves
-    // of 32 rows of one query head. In a batch that holds prefills, block
-    // decodes whose GQA group spans at least kPrefillQWaves query heads run
-    // in this launch too (kTileHeadsAcross tiles, n_fused_decode_tiles of
-    // n_prefill_tiles), filling its tail instead of a launch of their own.
+    // of 32 rows of one query head. In a batch that holds prefills (or a
+    // small decode-only batch), block decodes whose GQA group spans at least
+    // kPrefillQWaves query heads run in this launch too (kTileHeadsAcross
+    // tiles, n_fused_decode_tiles of n_prefill_tiles), filling its tail
+    // instead of a launch of their own.
     int32_t n_prefill_tiles;
     int32_t prefill_nb;
     int32_t n_merge_rows;

@@ -147,6 +147,25 @@ def test_block_decodes_fuse_into_prefill_launch():
         assert p3.info.num_fused_decode_tiles == 0
 
 
+def test_small_decode_only_gqa_batch_fuses():
+    # a decode-only batch of 28/4-head block decodes too small to fill the CUs
+    # takes heads-across tiles, its contexts cut to about two work-groups per
+    # CU; a large one keeps the whole-group decode tiles
+    for B, fused in ((1, True), (8, True), (16, True), (64, False)):
+        wl = workloads.decode_sweep("dream", B, 0)
+        p = plan_of(wl)
+        h, items, dec, pre, mer = parse(p)
+        if fused:
+            assert len(dec) == 0 and len(pre) == p.info.num_fused_decode_tiles > 0
+            assert np.all(pre["flags"] & HEADS_ACROSS)
+            n_tiles = sum(int(it["num_splits"]) for it in items) * wl.num_kv_heads * 2
+            assert len(pre) == n_tiles
+            assert 128 <= n_tiles <= 2 * 256 or B == 1
+            assert np.all(items["split_len"] >= 256)
+        else:
+            assert len(pre) == 0 and len(dec) > 0 and p.info.decode_q_waves == 7
+
+
 def test_splits_and_merge_rows():
     wl = workloads.make_workload("long", 0, hq=4, hkv=4, d=128,
                                  decodes=[(100, 9000), (0, 8192), (5, 300)], prefills=[20000])
