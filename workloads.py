@@ -369,12 +369,12 @@ def long_decode(seed: int = 0) -> Workload:
                          rng=rng, pool_pages=LONG_DECODE_POOL_PAGES)
 
 
-CONFIGS = {
-    0: tiny_mixed,
-    1: llada_decode,
-    2: dream_mixed,
-    3: prefill_heavy,
-    4: long_decode,
+WORKLOADS = {
+    "tiny_mixed": tiny_mixed,
+    "llada_decode": llada_decode,
+    "dream_mixed": dream_mixed,
+    "prefill_heavy": prefill_heavy,
+    "long_decode": long_decode,
 }
 
 
@@ -444,10 +444,6 @@ def decode_sweep(shape: str, batch: int, seed: int = 0, L: int = 1024) -> Worklo
     dec = [(L - 256 + 32 * int(b), L) for b in blocks]
     return make_workload(f"decode_sweep_{shape}_{batch}", seed, hq=hq, hkv=hkv, d=128, decodes=dec,
                          prefills=[], rng=rng)
-
-
-def by_index(idx: int, seed: int = 0) -> Workload:
-    return CONFIGS[idx](seed)
 
 
 def ragged_small(seed: int, *, hq: int, hkv: int, d: int, q_scale: float = 1.0) -> Workload:
