@@ -74,6 +74,9 @@ def make_desc(*, q_indptr, q_offset, kv_len, page_indptr, page_ids, num_q_heads,
     return d, arrays  # keep arrays alive while d is used
 
 
+_plan_cap = 1 << 16  # bytes of the first planning buffer; grows with the largest plan seen
+
+
 def plan(*, q_indptr, q_offset, kv_len, page_indptr, page_ids, num_q_heads, num_kv_heads, head_dim,
          num_pool_pages, sm_scale, page_size=16, force_kv_splits=0, num_cus=0, q_pos=None,
          device=None) -> Plan:
@@ -85,12 +88,18 @@ def plan(*, q_indptr, q_offset, kv_len, page_indptr, page_ids, num_q_heads, num_
                         num_kv_heads=num_kv_heads, head_dim=head_dim,
                         num_pool_pages=num_pool_pages, sm_scale=sm_scale, page_size=page_size,
                         force_kv_splits=force_kv_splits, num_cus=num_cus, q_pos=q_pos)
+    global _plan_cap
     used = ctypes.c_size_t(0)
-    st = lib.sangam_attn_plan(ctypes.byref(d), None, 0, ctypes.byref(used))
-    if st not in (_lib.SANGAM_OK, -5):  # -5: buffer too small, *used holds the size
-        check(st)
-    buf = np.zeros(int(used.value), np.uint8)
-    check(lib.sangam_attn_plan(ctypes.byref(d), buf.ctypes.data, buf.nbytes, ctypes.byref(used)))
+    # one planning pass in the common case: a buffer sized from earlier plans,
+    # a second pass only when this batch needs more (-5: *used holds the size)
+    buf = np.empty(_plan_cap, np.uint8)
+    st = lib.sangam_attn_plan(ctypes.byref(d), buf.ctypes.data, buf.nbytes, ctypes.byref(used))
+    if st == -5:
+        _plan_cap = max(_plan_cap, 2 * int(used.value))
+        buf = np.empty(int(used.value), np.uint8)
+        st = lib.sangam_attn_plan(ctypes.byref(d), buf.ctypes.data, buf.nbytes, ctypes.byref(used))
+    check(st)
+    buf = buf[:int(used.value)].copy() if buf.nbytes > 4 * int(used.value) else buf[:int(used.value)]
     info = PlanInfo()
     check(lib.sangam_plan_get_info(buf.ctypes.data, ctypes.byref(info)))
     del keep

@@ -8,6 +8,7 @@
 
 #include "../../include/sangam_kv.h"
 #include "kv_format.h"
+#include "page_check.h"
 
 namespace sangam {
 void set_error(const std::string& msg);
@@ -56,15 +57,12 @@ extern "C" sangam_status sangam_kv_plan(const sangam_kv_desc* d, void* plan_buf,
     if (rows > INT32_MAX) return kv_fail(SANGAM_ERR_INVALID_ARG, "more than 2^31 - 1 packed rows");
     const int64_t total_pages = d->page_indptr[n];
     // every page at most once: an import writes each listed page
-    std::vector<int32_t> sorted(d->page_ids, d->page_ids + total_pages);
-    for (int32_t pg : sorted)
-        if (pg < 0 || pg >= d->num_pool_pages)
-            return kv_fail(SANGAM_ERR_PAGE_RANGE, "page id " + std::to_string(pg) + " outside [0, " +
-                                                       std::to_string(d->num_pool_pages) + ")");
-    std::sort(sorted.begin(), sorted.end());
-    for (size_t k = 1; k < sorted.size(); ++k)
-        if (sorted[k] == sorted[k - 1])
-            return kv_fail(SANGAM_ERR_PAGE_ALIAS, "page " + std::to_string(sorted[k]) + " listed twice");
+    bool alias;
+    const int64_t bad = find_bad_page(d->page_ids, total_pages, d->num_pool_pages, &alias);
+    if (bad >= 0 && !alias)
+        return kv_fail(SANGAM_ERR_PAGE_RANGE, "page id " + std::to_string(d->page_ids[bad]) + " outside [0, " +
+                                                  std::to_string(d->num_pool_pages) + ")");
+    if (bad >= 0) return kv_fail(SANGAM_ERR_PAGE_ALIAS, "page " + std::to_string(d->page_ids[bad]) + " listed twice");
     const uint64_t off_pages = (sizeof(KvPlanHeader) + 255u) & ~uint64_t(255);
     const uint64_t total = off_pages + uint64_t(total_pages) * sizeof(KvPageRec);
     *used = size_t(total);

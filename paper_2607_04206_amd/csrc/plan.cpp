@@ -29,6 +29,7 @@
 #include <vector>
 
 #include "../../include/sangam_attn.h"
+#include "page_check.h"
 #include "plan_format.h"
 
 namespace sangam {
@@ -167,15 +168,13 @@ extern "C" sangam_status sangam_attn_plan(const sangam_attn_desc* d, void* plan_
     // ---- page ids: in range and never shared within the batch (two items
     // writing into one page would race)
     {
-        std::vector<int32_t> ids(d->page_ids, d->page_ids + total_pages);
-        for (int64_t k = 0; k < total_pages; ++k)
-            if (ids[k] < 0 || ids[k] >= d->num_pool_pages)
-                return fail(SANGAM_ERR_PAGE_RANGE, "page id " + std::to_string(ids[k]) + " at entry " +
-                                                       std::to_string(k) + " is outside the pool");
-        std::sort(ids.begin(), ids.end());
-        for (int64_t k = 1; k < total_pages; ++k)
-            if (ids[k] == ids[k - 1])
-                return fail(SANGAM_ERR_PAGE_ALIAS, "page id " + std::to_string(ids[k]) + " is listed twice");
+        bool alias;
+        const int64_t k = find_bad_page(d->page_ids, total_pages, d->num_pool_pages, &alias);
+        if (k >= 0 && !alias)
+            return fail(SANGAM_ERR_PAGE_RANGE, "page id " + std::to_string(d->page_ids[k]) + " at entry " +
+                                                   std::to_string(k) + " is outside the pool");
+        if (k >= 0)
+            return fail(SANGAM_ERR_PAGE_ALIAS, "page id " + std::to_string(d->page_ids[k]) + " is listed twice");
     }
 
     // ---- splits: decode-shaped contexts longer than kForcedSplitLen are always
@@ -300,6 +299,17 @@ extern "C" sangam_status sangam_attn_plan(const sangam_attn_desc* d, void* plan_
     // ---- tiles
     std::vector<TileRec> dec, pre;
     std::vector<int64_t> dec_cost, pre_cost;
+    {
+        int64_t nd = 0, np = 0;
+        for (int i = 0; i < n_items; ++i) {
+            const ItemRec& it = items[i];
+            if (it.n <= kWaveRows && fuse) np += int64_t(it.num_splits) * hkv * fused_tiles_per_kv_head;
+            else if (it.n <= kWaveRows) nd += int64_t(it.num_splits) * hkv * tiles_per_kv_head;
+            else np += int64_t(it.num_splits) * hq * ceil_div(it.n, kPrefillRows);
+        }
+        dec.reserve(size_t(nd)); dec_cost.reserve(size_t(nd));
+        pre.reserve(size_t(np)); pre_cost.reserve(size_t(np));
+    }
     int64_t n_fused = 0;  // (item, chunk) pairs cut into prefill-shaped tiles
     for (int i = 0; i < n_items; ++i) {
         const ItemRec& it = items[i];
@@ -334,12 +344,13 @@ extern "C" sangam_status sangam_attn_plan(const sangam_attn_desc* d, void* plan_
         }
     }
     // longest first (stable, so equal costs keep batch order)
+    // longest first, ties in creation order: one sort of (-cost, index) pairs
     auto lpt = [](std::vector<TileRec>& v, const std::vector<int64_t>& c) {
-        std::vector<size_t> idx(v.size());
-        std::iota(idx.begin(), idx.end(), 0);
-        std::stable_sort(idx.begin(), idx.end(), [&](size_t a, size_t b) { return c[a] > c[b]; });
+        std::vector<std::pair<int64_t, size_t>> key(v.size());
+        for (size_t k = 0; k < v.size(); ++k) key[k] = {-c[k], k};
+        std::sort(key.begin(), key.end());
         std::vector<TileRec> out(v.size());
-        for (size_t k = 0; k < idx.size(); ++k) out[k] = v[idx[k]];
+        for (size_t k = 0; k < key.size(); ++k) out[k] = v[key[k].second];
         v.swap(out);
     };
     lpt(dec, dec_cost);
