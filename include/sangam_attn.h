@@ -73,8 +73,11 @@ typedef struct sangam_attn_desc {
     int32_t num_kv_heads;    /* Hkv >= 1, Hq % Hkv == 0 */
     int32_t head_dim;        /* D: 64 or 128 */
     int32_t page_size;       /* tokens per KV page: 16 */
-    int32_t force_kv_splits; /* 0: the plan chooses; k >= 1: split every item's context
-                                into min(k, ceil(L_i / 64)) chunks (tests, tuning) */
+    int32_t force_kv_splits; /* 0: the plan chooses; k >= 1: cut every item's context into
+                                chunks of one 64-aligned length, round_up(ceil(L_i / k'), 64)
+                                with k' = min(k, ceil(L_i / 64)): at most k' chunks, at
+                                least two when k' >= 2 (more only where a tile's range
+                                limit of 8192 cached keys requires) (tests, tuning) */
     int64_t num_pool_pages;  /* pages in k_cache / v_cache */
     float sm_scale;          /* softmax scale, e.g. 1/sqrt(D) */
     int32_t num_cus;         /* compute units to balance over; 0 means 256 */
