@@ -210,11 +210,28 @@ __global__ __launch_bounds__(64 * QW * KW, MINB) void attn_tiles_kernel(AttnArgs
     const bool plist = (it.flags & kItemPosList) != 0;
     const int pg0 = kv_begin >> 4;
     if (!all_fresh) {
-        // the tile's page ids, once (the plan keeps such ranges <= kMaxCachedRange)
+        // the tile's page ids, once (the plan keeps such ranges <= kMaxCachedRange):
+        // every load is issued before the first LDS store, so a long range
+        // costs one memory round trip, not one per round of NT pages
         const int npg = ((kv_end + 15) >> 4) - pg0;
-        for (int k = tid; k < npg; k += NT) {
-            pages[k] = a.page_ids[it.page_start + pg0 + k];
-            if (plist) pinfo[k] = a.page_info[it.page_start + pg0 + k];
+        constexpr int PR = (MAX_PAGES + NT - 1) / NT;  // rounds of the page table per thread
+        int32_t pv[PR];
+        uint32_t iv[PR];
+#pragma unroll
+        for (int r = 0; r < PR; ++r) {
+            const int k = tid + r * NT;
+            if (k < npg) {
+                pv[r] = a.page_ids[it.page_start + pg0 + k];
+                if (plist) iv[r] = a.page_info[it.page_start + pg0 + k];
+            }
+        }
+#pragma unroll
+        for (int r = 0; r < PR; ++r) {
+            const int k = tid + r * NT;
+            if (k < npg) {
+                pages[k] = pv[r];
+                if (plist) pinfo[k] = iv[r];
+            }
         }
         if (plist && tid < it.n) fpos[tid] = a.positions[it.pos_start + tid];
     }
