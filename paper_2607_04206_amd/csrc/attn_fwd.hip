@@ -299,7 +299,7 @@ __global__ __launch_bounds__(64 * QW * KW, MINB) void attn_tiles_kernel(AttnArgs
         return key0 + STEP <= it.o || key0 >= it.o + it.n;
     };
 
-    auto issue_stage = [&](int st, int buf) {
+    auto issue_stage = [&](int st, int buf) __attribute__((always_inline)) {
         uint8_t* kb = smem + buf * 2 * TILE;
         uint8_t* vb = kb + TILE;
         const int key0 = kv_begin + st * STEP;
