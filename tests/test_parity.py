@@ -261,6 +261,22 @@ def test_deterministic(dev):
     assert torch.equal(o1, o2) and torch.equal(l1, l2)
 
 
+def test_forward_checks_pool_and_page_table(dev):
+    """The binding refuses a pool smaller than the plan's or a short device
+    page table before any launch (the kernels would read past them)."""
+    from paper_2607_04206_amd import attn
+    wl = workloads.ragged_small(4, hq=4, hkv=2, d=64)
+    t = workloads.device_inputs(wl, dev)
+    p = attn.plan(q_indptr=wl.q_indptr, q_offset=wl.q_offset, kv_len=wl.kv_len, page_indptr=wl.page_indptr,
+                  page_ids=wl.page_ids, num_q_heads=4, num_kv_heads=2, head_dim=64,
+                  num_pool_pages=wl.num_pool_pages, sm_scale=wl.sm_scale, device=dev)
+    small = t["k_cache"][: wl.num_pool_pages - 1]
+    with pytest.raises(ValueError, match="pool pages"):
+        attn.forward(p, t["q"], t["k_new"], t["v_new"], small, small, t["page_ids"])
+    with pytest.raises(ValueError, match="page_ids"):
+        attn.forward(p, t["q"], t["k_new"], t["v_new"], t["k_cache"], t["v_cache"], t["page_ids"][:-1])
+
+
 def test_graph_capture_replays(dev):
     """The forward is only kernel launches on the caller's stream, so a HIP
     graph can hold it: every replay (with eager work on the same buffers in
