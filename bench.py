@@ -101,9 +101,20 @@ def cpu_baseline(wl, budget_s):
     dt = time.perf_counter() - t
     n_dec = sum(1 for i in rows if wl.n(i) <= 32)
     n_pre_rows = sum(len(rows[i]) for i in rows if wl.n(i) > 32)
-    sample = (f"{n_dec} block decodes (all rows, all heads) and {n_pre_rows} evenly spaced "
-              f"prefill rows (all heads) of {wl.name} seed {wl.seed}: {acc / 1e9:.1f} GFLOP "
-              f"in {dt:.1f} s, fp64, input drawing excluded")
+    cpu = "unknown CPU"
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    cpu = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    total_pre_rows = sum(wl.n(i) for i in pre)
+    sample = (f"{n_dec} of {len(dec)} block decodes (all rows, all heads) and {n_pre_rows} of "
+              f"{total_pre_rows} prefill rows, evenly spaced (all heads), of {wl.name} seed {wl.seed}: "
+              f"{acc / 1e9:.1f} GFLOP in {dt:.1f} s, fp64, {threads} threads on {cpu}, "
+              f"input drawing excluded")
     return {"value": acc / dt / 1e12, "unit": "TFLOP/s", "cores": threads, "kind": "oracle",
             "sample": sample, "seconds": dt}
 
