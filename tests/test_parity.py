@@ -33,7 +33,7 @@ def dev():
     return torch.device("cuda:0")
 
 
-def run(wl, dev, force_splits=0, fill=float("nan"), want_lse=True):
+def run(wl, dev, force_splits=0, fill=float("nan"), want_lse=True, num_cus=0):
     from paper_2607_04206_amd import attn
     print(f"[case] {wl.name} seed={wl.seed} items={wl.num_items} force_splits={force_splits}",
           flush=True)
@@ -42,7 +42,7 @@ def run(wl, dev, force_splits=0, fill=float("nan"), want_lse=True):
                   page_indptr=wl.page_indptr, page_ids=wl.page_ids, num_q_heads=wl.num_q_heads,
                   num_kv_heads=wl.num_kv_heads, head_dim=wl.head_dim,
                   num_pool_pages=wl.num_pool_pages, sm_scale=wl.sm_scale,
-                  force_kv_splits=force_splits, q_pos=wl.q_pos, device=dev)
+                  force_kv_splits=force_splits, q_pos=wl.q_pos, num_cus=num_cus, device=dev)
     out, lse = attn.forward(p, t["q"], t["k_new"], t["v_new"], t["k_cache"], t["v_cache"],
                             t["page_ids"], want_lse=want_lse)
     torch.cuda.synchronize()
@@ -220,6 +220,25 @@ def test_long_decode(dev):
     assert int(wl.kv_len[order[0]]) > 8192  # split-KV path exercised
     check_sampled(wl, out, lse, items=items, heads=[0, 13, 31])
     check_cache(wl, t, items=items)
+    check_pool_untouched(wl, t)
+
+
+@pytest.mark.parametrize("hq,hkv,with_prefill,cus", [(8, 8, False, 0), (28, 4, False, 0), (28, 4, False, 8),
+                                                     (28, 4, True, 0)])
+def test_range_limit_boundary(dev, hq, hkv, with_prefill, cus):
+    """Contexts at the longest range a tile may read from the cache (8192
+    keys: 512 staged page ids, unsplit when one chunk per item is asked for)
+    and one key past it (cut in two), block offsets at both ends; every row
+    of these items against the oracle."""
+    wl = workloads.make_workload("range_limit", 21, hq=hq, hkv=hkv, d=128,
+                                 decodes=[(8192 - 32, 8192), (0, 8192), (8192 - 20, 8193), (4000, 8193)],
+                                 prefills=[200] if with_prefill else [])
+    p, t, out, lse = run(wl, dev, force_splits=1, num_cus=cus)
+    assert [len(p.item_splits(i)) - 1 for i in range(4)] == [1, 1, 2, 2]
+    # the MHA case and the 8-CU GQA case run decode-shaped tiles, the others heads-across tiles
+    assert (p.info.num_decode_tiles > 0) == (hq == hkv or cus == 8)
+    check_sampled(wl, out, lse, items=list(range(4)), heads=[0, hq // 2, hq - 1])
+    check_cache(wl, t)
     check_pool_untouched(wl, t)
 
 
