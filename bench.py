@@ -206,7 +206,9 @@ def decode_sweep(args):
                 "kernel_mfma_frac": F / (kern / 1e3) / (PEAK_BF16_TFLOPS * 1e12),
                 "decode_launch": "prefill-shaped (heads across)" if fused else "decode-shaped",
                 "splits": int(p.info.num_split_items),
-                "tiles": int(p.info.num_prefill_tiles if fused else p.info.num_decode_tiles)}), flush=True)
+                "tiles": int(p.info.num_prefill_tiles if fused else p.info.num_decode_tiles),
+                "cpu_baseline": None if args.no_cpu_baseline else cpu_baseline(wl, args.sweep_cpu_budget)}),
+                  flush=True)
             del t, out, lse, ws
 
 
@@ -250,6 +252,42 @@ def serve_trace(args):
         "plan_ms_mean": float(np.mean([r.plan_ms for r in log])),
     }
     print(json.dumps(res), flush=True)
+
+
+def kv_cpu_baseline(pool_k, pool_v, kv_len, page_indptr, page_ids, hkv, d, budget_s):
+    """The export oracle (as it stands, one position at a time) on the first
+    requests of the batch, as many as take about budget_s; their pages are
+    copied to host memory first (not timed). Rate in the GPU lines' unit:
+    K and V of every exported position read once and written once."""
+    import numpy as np
+    import torch
+
+    from oracle import kv_transfer as okv
+
+    def sample(n_req):
+        lens = [int(x) for x in kv_len[:n_req]]
+        pages = page_ids[page_indptr[0]:page_indptr[n_req]]
+        idx = torch.as_tensor(pages.astype(np.int64), device=pool_k.device)
+        hk = pool_k.index_select(0, idx).view(torch.int16).cpu().numpy()
+        hv = pool_v.index_select(0, idx).view(torch.int16).cpu().numpy()
+        local = np.arange(len(pages), dtype=np.int64)  # pages renumbered in sample order
+        ind = np.asarray(page_indptr[:n_req + 1], np.int64) - int(page_indptr[0])
+        t = time.perf_counter()
+        okv.export(hk, hv, lens, ind, local)
+        return sum(lens), time.perf_counter() - t
+
+    rows1, dt1 = sample(1)
+    per_row = dt1 / max(rows1, 1)
+    n_req, acc = 0, 0
+    while n_req < len(kv_len) and (acc + int(kv_len[n_req])) * per_row <= budget_s:
+        acc += int(kv_len[n_req])
+        n_req += 1
+    n_req = max(n_req, 1)
+    rows, dt = sample(n_req)
+    moved = 2 * 2 * rows * hkv * d * 2
+    return {"value": moved / dt / 1e9, "unit": "GB/s", "cores": 1, "kind": "oracle",
+            "sample": f"export of {rows} positions ({n_req} of {len(kv_len)} requests) in {dt:.2f} s, "
+                      f"pure Python, one thread"}
 
 
 def kv_transfer(args):
@@ -307,6 +345,8 @@ def kv_transfer(args):
             res[f"{op}_gbs"] = moved / (us / 1e6) / 1e9
             res[f"{op}_hbm_frac"] = res[f"{op}_gbs"] / PEAK_HBM_GBS
         res["bytes_moved_per_copy"] = moved
+        if not args.no_cpu_baseline:
+            res["cpu_baseline"] = kv_cpu_baseline(ka, va, wl.kv_len, indptr, src, hkv, d, args.kv_cpu_budget)
         print(json.dumps(res), flush=True)
         del ka, va, kb, vb, pk, pv
         torch.cuda.empty_cache()
@@ -323,6 +363,10 @@ def main():
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle work")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--sweep-cpu-budget", type=float, default=1.0,
+                    help="seconds of oracle work per point (--decode-sweep)")
+    ap.add_argument("--kv-cpu-budget", type=float, default=2.0,
+                    help="seconds of oracle work per batch (--kv-transfer)")
     ap.add_argument("--copy-calib-mib", type=int, default=0,
                     help="run one device-to-device copy of this many MiB before warm-up, as the "
                          "reference kernel that scales the HBM traffic counters")
