@@ -234,15 +234,16 @@ extern "C" sangam_status sangam_attn_plan(const sangam_attn_desc* d, void* plan_
     chunk = std::min<int64_t>(std::max<int64_t>(round_up(std::max<int64_t>(chunk, 1), kKeyAlign),
                                                 underfilled ? min_chunk_idle(qw) : min_chunk(qw)),
                               kForcedSplitLen);
-    if (underfilled && qw > 1) {
-        // A split of a GQA block decode writes partial O for all G query
-        // heads of the group (and the merge reads it back): for the Dream
-        // shape that is about as many bytes as the chunk's K/V. So an
-        // underfilled GQA launch is cut only as far as one work-group per
-        // CU: the shortest chunk (from min_chunk_idle up, in kKeyAlign
-        // steps) whose tiles fit in num_cus (measured on 28/4 heads: 48
-        // Dream decodes 50 instead of 63 µs, 32 decodes of 1024 keys
-        // unchanged).
+    if (underfilled) {
+        // Cutting further than the work-groups the chip keeps resident (two
+        // MHA or one GQA whole-group work-group per CU) only adds merge work
+        // and per-tile start-up: the chunk is the shortest (from the floor
+        // above, in kKeyAlign steps) whose tiles fit in those slots. A split
+        // of a GQA block decode also writes partial O for all G query heads
+        // of the group, about as many bytes as the chunk's K/V for the Dream
+        // shape. (Measured: 6-15 LLaDA decodes of 1024 keys 17-30 % faster,
+        // 48 Dream decodes 50 instead of 63 us, 1-4 and 32 decodes unchanged.)
+        const int64_t slots = int64_t(num_cus) * (qw == 1 ? 2 : 1);
         auto tiles_at = [&](int64_t c) {
             int64_t n = 0;
             for (int i = 0; i < n_items; ++i)
@@ -250,12 +251,12 @@ extern "C" sangam_status sangam_attn_plan(const sangam_attn_desc* d, void* plan_
                     n += int64_t(hkv) * tiles_per_kv_head * ceil_div(d->kv_len[i], c);
             return n;
         };
-        int64_t lo = chunk, hi = kForcedSplitLen;  // tiles_at(hi) <= num_cus: the launch is underfilled
-        if (tiles_at(lo) > int64_t(num_cus)) {
-            while (hi - lo > kKeyAlign) {  // invariant: tiles_at(lo) > num_cus >= tiles_at(hi)
+        int64_t lo = chunk, hi = kForcedSplitLen;  // tiles_at(hi) <= slots: the launch is underfilled
+        if (tiles_at(lo) > slots) {
+            while (hi - lo > kKeyAlign) {  // invariant: tiles_at(lo) > slots >= tiles_at(hi)
                 const int64_t mid = round_up((lo + hi) / 2, kKeyAlign);
                 if (mid >= hi) break;
-                if (tiles_at(mid) > int64_t(num_cus)) lo = mid;
+                if (tiles_at(mid) > slots) lo = mid;
                 else hi = mid;
             }
             chunk = hi;

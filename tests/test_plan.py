@@ -166,11 +166,11 @@ def test_small_decode_only_gqa_batch_fuses():
             assert len(pre) == 0 and len(dec) > 0 and p.info.decode_q_waves == 7
 
 
-def test_underfilled_gqa_decode_launch_cut_to_one_work_group_per_cu():
-    # a decode-only GQA batch too big for heads-across tiles but with fewer
-    # whole-group tiles than CUs is cut with the shortest chunk (>= 512 keys,
-    # 64-aligned) that keeps its tiles within the CU count: each split writes
-    # partial O for all query heads of the group
+def test_underfilled_decode_launch_cut_to_resident_work_groups():
+    # a decode-only batch whose whole-context tiles leave resident slots idle
+    # (two MHA or one GQA whole-group work-group per CU) is cut with the
+    # shortest chunk (from the floor: 256 keys MHA, 512 GQA; 64-aligned)
+    # whose tiles still fit in those slots
     def cdiv(a, b):
         return -(-a // b)
 
@@ -181,17 +181,23 @@ def test_underfilled_gqa_decode_launch_cut_to_one_work_group_per_cu():
     dec = [(int(base.q_offset[i]), int(base.kv_len[i])) for i in range(base.num_items) if not base.is_prefill[i]]
     cases = [(workloads.make_workload("dreamdec", 0, hq=28, hkv=4, d=128, decodes=dec, prefills=[]), 256),
              (workloads.decode_sweep("dream", 32, 0), 256), (workloads.decode_sweep("dream", 32, 0), 200)]
+    cases += [(workloads.decode_sweep("llada", B, 0), 256) for B in (1, 6, 8, 12, 15)]
     for wl, cus in cases:
         p = plan_of(wl, num_cus=cus)
         h, items, dec_t, pre, mer = parse(p)
-        assert len(pre) == 0 and p.info.decode_q_waves == 7
-        assert wl.num_items * wl.num_kv_heads < cus  # underfilled without splits
-        chunk = next(c for c in range(512, 8192 + 1, 64) if tiles_at(wl, c) <= cus)
+        mha = wl.num_q_heads == wl.num_kv_heads
+        assert len(pre) == 0 and p.info.decode_q_waves == (1 if mha else 7)
+        slots = cus * (2 if mha else 1)
+        assert wl.num_items * wl.num_q_heads // p.info.decode_q_waves < slots  # underfilled without splits
+        floor = 256 if mha else 512
+        chunk = max(floor, next(c for c in range(floor, 8192 + 1, 64) if tiles_at(wl, c) <= slots))
         for it, L in zip(items, wl.kv_len):
             pieces = cdiv(int(L), chunk)
             length = 64 * cdiv(cdiv(int(L), pieces), 64)  # 64-aligned piece length
             assert int(it["num_splits"]) == cdiv(int(L), length), (int(L), chunk)
-        assert len(dec_t) == sum(wl.num_kv_heads * int(it["num_splits"]) for it in items) <= cus
+        assert len(dec_t) == sum(wl.num_kv_heads * int(it["num_splits"]) for it in items) <= slots
+    # one LLaDA decode still takes its four 256-key pieces (the floor binds)
+    assert plan_of(workloads.decode_sweep("llada", 1, 0), num_cus=256).info.num_decode_tiles == 4 * 32
     # the uniform 32-decode batch keeps its two pieces per context at 256 CUs
     p = plan_of(workloads.decode_sweep("dream", 32, 0), num_cus=256)
     assert p.info.num_split_items == 32 and p.info.num_decode_tiles == 256
