@@ -231,6 +231,7 @@ def serve_trace(args):
     log = loop.run(args.trace_iters * 8)
     torch.cuda.synchronize()
     ms = np.asarray([r.events[0].elapsed_time(r.events[1]) for r in log])
+    kern = np.asarray([sum(a.elapsed_time(b) for a, b in r.launch_events) for r in log])
     mixed = np.asarray([r.prefills > 0 for r in log])
     waits = [w for r in log for w in r.queue_waits]
     def pct(x, q):
@@ -244,6 +245,11 @@ def serve_trace(args):
         "decode_only_ms_mean": float(ms[~mixed].mean()) if (~mixed).any() else None,
         "mixed_ms_mean": float(ms[mixed].mean()) if mixed.any() else None,
         "mixed_ms_p99": pct(ms[mixed], 99),
+        # the same from events in the launches' dispatches: kernel time, no host gaps
+        "kernel_ms_mean": float(kern.mean()), "kernel_ms_p99": pct(kern, 99),
+        "decode_only_kernel_ms_mean": float(kern[~mixed].mean()) if (~mixed).any() else None,
+        "mixed_kernel_ms_mean": float(kern[mixed].mean()) if mixed.any() else None,
+        "mixed_kernel_ms_p99": pct(kern[mixed], 99),
         "prefill_tokens_per_busy_iteration": float(np.mean([r.prefill_tokens for r in log])),
         "prefill_tokens_max": int(max(r.prefill_tokens for r in log)),
         "decodes_mean": float(np.mean([r.decodes for r in log])),

@@ -6,7 +6,7 @@ from __future__ import annotations
 
 import ctypes
 from dataclasses import dataclass
-from typing import Optional, Tuple
+from typing import Optional, Tuple, Sequence
 
 import numpy as np
 import torch
@@ -129,9 +129,13 @@ def forward(p: Plan, q: torch.Tensor, k_new: torch.Tensor, v_new: torch.Tensor,
             k_cache: torch.Tensor, v_cache: torch.Tensor, page_ids: torch.Tensor,
             out: Optional[torch.Tensor] = None, lse: Optional[torch.Tensor] = None,
             workspace: Optional[torch.Tensor] = None, want_lse: bool = True,
-            stream: Optional[torch.cuda.Stream] = None) -> Tuple[torch.Tensor, Optional[torch.Tensor]]:
+            stream: Optional[torch.cuda.Stream] = None,
+            launch_events: Optional[Sequence[torch.cuda.Event]] = None) -> Tuple[torch.Tensor, Optional[torch.Tensor]]:
     """sangam_attn_forward on the current (or given) stream. Allocates out,
-    lse and the workspace with torch when they are not passed."""
+    lse and the workspace with torch when they are not passed. With six
+    timing events, calls sangam_attn_forward_timed instead: events 2k and
+    2k + 1 travel in the dispatch of launch k (prefill-shaped, decode-shaped,
+    merge), so their elapsed time is that kernel's execution alone."""
     dev = q.device
     if dev.type != "cuda":
         raise ValueError("forward needs device tensors (a ROCm GPU)")
@@ -164,9 +168,14 @@ def forward(p: Plan, q: torch.Tensor, k_new: torch.Tensor, v_new: torch.Tensor,
     ws_ptr = workspace.data_ptr() if workspace is not None else None
     ws_len = workspace.numel() * workspace.element_size() if workspace is not None else 0
     s = stream if stream is not None else torch.cuda.current_stream(dev)
-    check(lib.sangam_attn_forward(p.host_ptr(), p.dev.data_ptr(), q.data_ptr(), k_new.data_ptr(),
-                                  v_new.data_ptr(), k_cache.data_ptr(), v_cache.data_ptr(),
-                                  page_ids.data_ptr(), out.data_ptr(),
-                                  lse.data_ptr() if lse is not None else None, ws_ptr, ws_len,
-                                  s.cuda_stream))
+    args = (p.host_ptr(), p.dev.data_ptr(), q.data_ptr(), k_new.data_ptr(), v_new.data_ptr(),
+            k_cache.data_ptr(), v_cache.data_ptr(), page_ids.data_ptr(), out.data_ptr(),
+            lse.data_ptr() if lse is not None else None, ws_ptr, ws_len, s.cuda_stream)
+    if launch_events is None:
+        check(lib.sangam_attn_forward(*args))
+    else:
+        if len(launch_events) != 6:
+            raise ValueError("launch_events needs 6 events (start and stop of 3 launches)")
+        evs = (ctypes.c_void_p * 6)(*[e.cuda_event for e in launch_events])
+        check(lib.sangam_attn_forward_timed(*args, evs))
     return out, lse

@@ -68,6 +68,9 @@ class Iteration:
     deficit: int
     plan_ms: float
     events: Optional[tuple] = None  # (start, end) torch events around the call
+    # start / stop events in the dispatch of each launch that ran (prefill-
+    # shaped, decode-shaped, merge): kernel execution without host gaps
+    launch_events: Optional[list] = None
     queue_waits: List[int] = dataclasses.field(default_factory=list)
     captured: Optional[dict] = None
     batch: Optional[list] = None  # (request id, kind) of each item, in batch order
@@ -153,6 +156,7 @@ class ServingLoop:
         rec = Iteration(t=t, decodes=len(decodes), prefills=len(admitted),
                         prefill_tokens=int(sum(s.L for s in admitted)), waiting_after=len(self.waiting),
                         deficit=self.deficit, plan_ms=plan_ms, events=self._ev if timed else None,
+                        launch_events=self._lev if timed else None,
                         queue_waits=[t - s.queued_at for s in admitted])
         rec.captured = self._snap if capture else None
         rec.batch = [(s.req.rid, "decode" if k < nd else "prefill") for k, s in enumerate(items)]
@@ -172,18 +176,24 @@ class ServingLoop:
                         v_new=self.v_new[:rows].clone(),
                         k_pages=self.k_cache[pid.long()].clone(), v_pages=self.v_cache[pid.long()].clone(),
                         decodes=nd)
-        ev = None
+        ev = lev = used = None
         if timed:
             ev = (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+            lev = [torch.cuda.Event(enable_timing=True) for _ in range(6)]
+            for e in lev:  # torch reads elapsed time only from events it has recorded
+                e.record(stream)
+            i = p.info
+            used = (i.num_prefill_tiles > 0, i.num_decode_tiles > 0, i.num_split_items > 0)
             ev[0].record(stream)
         attn.forward(p, self.q[:rows], self.k_new[:rows], self.v_new[:rows], self.k_cache, self.v_cache,
-                     pid, out=self.out[:rows], lse=self.lse[:rows])
+                     pid, out=self.out[:rows], lse=self.lse[:rows], launch_events=lev)
         if timed:
             ev[1].record(stream)
+            lev = [(lev[2 * k], lev[2 * k + 1]) for k in range(3) if used[k]]
         if capture:
             snap["out"] = self.out[:rows].clone()
             snap["lse"] = self.lse[:rows].clone()
-        self._ev, self._snap = ev, snap
+        self._ev, self._lev, self._snap = ev, lev, snap
 
     def _advance(self, t, decodes, admitted):
         # advance: a prefill starts (or resumes at) its block; a decode step
