@@ -280,6 +280,30 @@ def test_deterministic(dev):
     assert torch.equal(o1, o2) and torch.equal(l1, l2)
 
 
+def test_forward_with_launch_events(dev):
+    """The timed entry point (events in each launch's dispatch) computes the
+    same bits as the plain one, and each launch that ran reports a positive
+    execution time."""
+    from paper_2607_04206_amd import attn
+    wl = workloads.ragged_small(3, hq=8, hkv=2, d=128)
+    p, t, out0, lse0 = run(wl, dev, force_splits=2)
+    stream = torch.cuda.current_stream(dev)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(6)]
+    for e in ev:
+        e.record(stream)
+    out, lse = attn.forward(p, t["q"], t["k_new"], t["v_new"], t["k_cache"], t["v_cache"], t["page_ids"],
+                            launch_events=ev)
+    torch.cuda.synchronize()
+    assert torch.equal(out, out0) and torch.equal(lse, lse0)
+    i = p.info
+    for k, ran in enumerate((i.num_prefill_tiles > 0, i.num_decode_tiles > 0, i.num_split_items > 0)):
+        if ran:
+            assert ev[2 * k].elapsed_time(ev[2 * k + 1]) > 0.0
+    with pytest.raises(ValueError, match="6 events"):
+        attn.forward(p, t["q"], t["k_new"], t["v_new"], t["k_cache"], t["v_cache"], t["page_ids"],
+                     launch_events=ev[:4])
+
+
 def test_forward_checks_pool_and_page_table(dev):
     """The binding refuses a pool smaller than the plan's or a short device
     page table before any launch (the kernels would read past them)."""
