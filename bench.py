@@ -158,7 +158,7 @@ def decode_sweep(args):
     dev = torch.device("cuda:0")
     stream = torch.cuda.current_stream(dev)
     for shape in ("llada", "dream"):
-        for B in (1, 2, 4, 8, 16, 32, 64):
+        for B in [int(b) for b in args.sweep_batches.split(",")]:
             wl = workloads.decode_sweep(shape, B, args.seed)
             t = workloads.device_inputs(wl, dev, fill=None)
             p = attn.plan(q_indptr=wl.q_indptr, q_offset=wl.q_offset, kv_len=wl.kv_len,
@@ -364,11 +364,13 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="dream_mixed",
-                    choices=["tiny_mixed", "llada_decode", "dream_mixed", "prefill_heavy", "long_decode",
-                             "token_cache"])
+                    choices=["tiny_mixed", "llada_decode", "dream_mixed", "dream_decode", "prefill_heavy",
+                             "long_decode", "token_cache"])
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle work")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--sweep-batches", default="1,2,4,8,16,32,64",
+                    help="comma-separated batch sizes (--decode-sweep)")
     ap.add_argument("--sweep-cpu-budget", type=float, default=1.0,
                     help="seconds of oracle work per point (--decode-sweep)")
     ap.add_argument("--kv-cpu-budget", type=float, default=2.0,

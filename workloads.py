@@ -346,6 +346,16 @@ def dream_mixed(seed: int = 0) -> Workload:
                          prefills=[2304, 3328], rng=rng)
 
 
+def dream_decode(seed: int = 0) -> Workload:
+    """The 48 block decodes of dream_mixed(seed) alone (the same lengths and
+    block offsets; GQA 28/4, D 128): a decode-only batch whose whole-group
+    tiles leave CUs idle unless its contexts are cut."""
+    rng = np.random.default_rng(seed)
+    P = _lognormal_lengths(rng, 48, 500, 0.8, 16, 4096)
+    dec = _decodes_from_prompts(rng, P, 256)
+    return make_workload("dream_decode", seed, hq=28, hkv=4, d=128, decodes=dec, prefills=[], rng=rng)
+
+
 def prefill_heavy(seed: int = 0) -> Workload:
     """Long-document prefills: GQA 28/4, D 128; 8 whole prefills with prompts
     ~ LN(6000, 0.5) in [1024, 16384] + 256 response; KV written to pages."""
@@ -373,6 +383,7 @@ WORKLOADS = {
     "tiny_mixed": tiny_mixed,
     "llada_decode": llada_decode,
     "dream_mixed": dream_mixed,
+    "dream_decode": dream_decode,
     "prefill_heavy": prefill_heavy,
     "long_decode": long_decode,
 }
