@@ -65,14 +65,14 @@ static int decode_kv_waves(int qw) {
     return 1;
 }
 
-// Shortest context chunk the planner cuts for balance (forced splits above
-// kForcedSplitLen aside): a chunk must carry enough keys to amortize a
-// work-group's prologue and its merge traffic. A GQA work-group does G times
-// the work per key, so it tolerates shorter chunks; but each of its chunks
-// also writes (and the merge reads back) a G x 32-row fp32 partial, which
-// below about 1024 keys costs more than the balance gains (measured on
-// block decodes of 28/4 heads).
-static int64_t min_chunk(int qw) { return qw == 1 ? 2048 : 1024; }
+// Shortest context chunk the planner cuts for balance in a launch that fills
+// the CUs (forced splits above kForcedSplitLen aside): a chunk must carry
+// enough keys to amortize a work-group's prologue and its merge traffic. A
+// GQA chunk also writes (and the merge reads back) a G x 32-row fp32 partial,
+// about the bytes of 1024 keys of its K/V at G = 7, so GQA takes the same
+// floor as MHA (measured on 96 Dream decodes of 28/4 heads: 79 us with 2048,
+// 82-99 us with 1024, 102-135 us with no balance split).
+static int64_t min_chunk(int /*qw*/) { return 2048; }
 // the same floor while a decode launch leaves CUs idle (see below)
 static int64_t min_chunk_idle(int qw) { return qw == 1 ? 256 : 512; }
 
