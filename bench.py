@@ -169,10 +169,8 @@ def decode_sweep(args):
             out = torch.empty((wl.total_q, wl.num_q_heads, wl.head_dim), dtype=torch.bfloat16, device=dev)
             lse = torch.empty((wl.total_q, wl.num_q_heads), dtype=torch.float32, device=dev)
             ws = torch.empty((max(p.workspace_bytes, 16),), dtype=torch.uint8, device=dev)
-            args_c = [p.host_ptr(), p.dev.data_ptr(), t["q"].data_ptr(), t["k_new"].data_ptr(),
-                      t["v_new"].data_ptr(), t["k_cache"].data_ptr(), t["v_cache"].data_ptr(),
-                      t["page_ids"].data_ptr(), out.data_ptr(), lse.data_ptr(), ws.data_ptr(), ws.numel(),
-                      stream.cuda_stream]
+            args_c = attn.c_args(p, t["q"], t["k_new"], t["v_new"], t["k_cache"], t["v_cache"],
+                                 t["page_ids"], out, lse, ws, stream)
             for _ in range(args.warmup):
                 check(lib.sangam_attn_forward(*args_c))
             K = args.steps
@@ -435,10 +433,8 @@ def main():
     ws = torch.empty((max(p.workspace_bytes, 16),), dtype=torch.uint8, device=dev)
     stream = torch.cuda.current_stream(dev)
     import ctypes
-    args_c = [p.host_ptr(), p.dev.data_ptr(), t["q"].data_ptr(), t["k_new"].data_ptr(),
-              t["v_new"].data_ptr(), t["k_cache"].data_ptr(), t["v_cache"].data_ptr(),
-              t["page_ids"].data_ptr(), out.data_ptr(), lse.data_ptr(), ws.data_ptr(), ws.numel(),
-              stream.cuda_stream]
+    args_c = attn.c_args(p, t["q"], t["k_new"], t["v_new"], t["k_cache"], t["v_cache"], t["page_ids"],
+                         out, lse, ws, stream)
 
     def make_events(which=range(3)):
         """Start / stop event pairs of the three launches; launches outside

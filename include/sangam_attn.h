@@ -142,17 +142,21 @@ sangam_status sangam_plan_item_splits(const void *plan_buf, int32_t item, int32_
  * synchronizes and copies nothing between host and device, so it may be
  * captured into a HIP graph. plan_host is the plan in host memory (launch
  * sizes are read from it); plan_dev is the same bytes in device memory.
- * page_ids_dev holds desc->page_ids in device memory. lse may be NULL.
- * workspace must hold sangam_plan_workspace_bytes(plan_host) bytes (NULL
- * when that is 0); workspace_bytes is its size.
+ * k_cache / v_cache each hold pool_pages pages of [Hkv, 16, D] bf16; the
+ * kernels address pages below the plan's num_pool_pages, so pool_pages must
+ * be at least that. page_ids_dev holds desc->page_ids in device memory,
+ * num_page_ids entries of it (at least page_indptr[num_items]). lse may be
+ * NULL. workspace must hold sangam_plan_workspace_bytes(plan_host) bytes
+ * (NULL when that is 0); workspace_bytes is its size.
  * Errors: SANGAM_ERR_PLAN, _INVALID_ARG (a NULL tensor), _ALIGN, _BUFFER
- * (workspace too small), _HIP (launch failed; nothing is rolled back).
+ * (workspace, pool or page table smaller than the plan addresses), _HIP
+ * (launch failed; nothing is rolled back).
  */
 sangam_status sangam_attn_forward(const void *plan_host, const void *plan_dev, const void *q,
                                   const void *k_new, const void *v_new, void *k_cache,
-                                  void *v_cache, const int32_t *page_ids_dev, void *out,
-                                  float *lse, void *workspace, size_t workspace_bytes,
-                                  void *stream);
+                                  void *v_cache, int64_t pool_pages, const int32_t *page_ids_dev,
+                                  int64_t num_page_ids, void *out, float *lse, void *workspace,
+                                  size_t workspace_bytes, void *stream);
 
 /*
  * sangam_attn_forward, plus HIP events carried by its launches, for measuring
@@ -169,7 +173,8 @@ sangam_status sangam_attn_forward(const void *plan_host, const void *plan_dev, c
  */
 sangam_status sangam_attn_forward_timed(const void *plan_host, const void *plan_dev,
                                         const void *q, const void *k_new, const void *v_new,
-                                        void *k_cache, void *v_cache, const int32_t *page_ids_dev,
+                                        void *k_cache, void *v_cache, int64_t pool_pages,
+                                        const int32_t *page_ids_dev, int64_t num_page_ids,
                                         void *out, float *lse, void *workspace,
                                         size_t workspace_bytes, void *stream,
                                         void *const *events);

@@ -69,9 +69,19 @@ def _bits(t) -> np.ndarray:
 class Call:
     """Packed arrays of one oracle call (a subset of a workload's items)."""
 
-    def __init__(self, wl, items: Optional[Sequence[int]] = None):
+    def __init__(self, wl, items: Optional[Sequence[int]] = None, heads: Optional[Sequence[int]] = None):
+        """heads: optional query heads; the call then holds only those (in that
+        order), each paired with its own copy of its KV head g = h // G
+        (G = 1 in the reduced call), so every (row, head) result is the one
+        of the full call, without drawing the other heads' values."""
         self.items = list(range(wl.num_items)) if items is None else list(items)
         self.hq, self.hkv, self.d = wl.num_q_heads, wl.num_kv_heads, wl.head_dim
+        qh = kvh = None
+        if heads is not None:
+            G = wl.num_q_heads // wl.num_kv_heads
+            qh = [int(h) for h in heads]
+            kvh = [h // G for h in qh]
+            self.hq = self.hkv = len(qh)
         self.sm_scale = wl.sm_scale
         n = [wl.n(i) for i in self.items]
         self.q_indptr = np.zeros(len(n) + 1, np.int32)
@@ -84,17 +94,17 @@ class Call:
         self.kv_len = np.asarray([wl.kv_len[i] for i in self.items], np.int32)
         z = np.zeros((0,), np.uint16)
         empty = (lambda: z)
-        self.q = np.concatenate([_bits(wl.q(i)).reshape(-1) for i in self.items] or [empty()])
-        self.k_new = np.concatenate([_bits(wl.k_new(i)).reshape(-1) for i in self.items] or [empty()])
-        self.v_new = np.concatenate([_bits(wl.v_new(i)).reshape(-1) for i in self.items] or [empty()])
+        self.q = np.concatenate([_bits(wl.q(i, heads=qh)).reshape(-1) for i in self.items] or [empty()])
+        self.k_new = np.concatenate([_bits(wl.k_new(i, heads=kvh)).reshape(-1) for i in self.items] or [empty()])
+        self.v_new = np.concatenate([_bits(wl.v_new(i, heads=kvh)).reshape(-1) for i in self.items] or [empty()])
         kc, vc, ctx = [], [], [0]
         for i in self.items:
-            k = wl.k_ctx(i)
+            k = wl.k_ctx(i, heads=kvh)
             if k is None:
                 ctx.append(ctx[-1])
                 continue
             kc.append(_bits(k).reshape(-1))
-            vc.append(_bits(wl.v_ctx(i)).reshape(-1))
+            vc.append(_bits(wl.v_ctx(i, heads=kvh)).reshape(-1))
             ctx.append(ctx[-1] + int(wl.kv_len[i]))
         self.ctx_indptr = np.asarray(ctx, np.int64)
         self.k_ctx = np.concatenate(kc) if kc else np.zeros((1,), np.uint16)
@@ -144,8 +154,9 @@ def attention(wl, items: Optional[Sequence[int]] = None,
     heads: optional list of query heads; default all.
     Returns {item: (local_rows, out [len(rows), len(heads), D], lse [len(rows), len(heads)])}.
     """
-    call = Call(wl, items)
-    sel, layout, hs = selection(call, rows, heads)
+    # only the chosen heads' values are drawn (the reduced call holds them in order)
+    call = Call(wl, items, heads=heads)
+    sel, layout, hs = selection(call, rows, None)
     out, lse = run(call, sel)
     res = {}
     for i, (rr, base) in layout.items():

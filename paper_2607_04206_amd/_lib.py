@@ -121,9 +121,10 @@ def _load():
     lib.sangam_deficit_admit.argtypes = [ctypes.c_int64, ctypes.c_int64, ctypes.c_int32, P, ctypes.c_int32,
                                          i64p, ctypes.POINTER(ctypes.c_int32)]
     lib.sangam_deficit_admit.restype = ctypes.c_int32
-    lib.sangam_attn_forward.argtypes = [P, P, P, P, P, P, P, P, P, P, P, S, P]
+    I64 = ctypes.c_int64
+    lib.sangam_attn_forward.argtypes = [P, P, P, P, P, P, P, I64, P, I64, P, P, P, S, P]
     lib.sangam_attn_forward.restype = ctypes.c_int32
-    lib.sangam_attn_forward_timed.argtypes = [P, P, P, P, P, P, P, P, P, P, P, S, P, P]
+    lib.sangam_attn_forward_timed.argtypes = [P, P, P, P, P, P, P, I64, P, I64, P, P, P, S, P, P]
     lib.sangam_attn_forward_timed.restype = ctypes.c_int32
     lib.sangam_kv_plan.argtypes = [ctypes.POINTER(KvDesc), P, S, ctypes.POINTER(S)]
     lib.sangam_kv_plan.restype = ctypes.c_int32

@@ -47,9 +47,14 @@ class Plan:
         return starts
 
     def to(self, device) -> "Plan":
-        """Copy the blob to device memory (the caller's H2D copy of plan_dev)."""
-        t = torch.from_numpy(self.host)
-        self.dev = t.to(device)
+        """Copy the blob to device memory (the caller's H2D copy of plan_dev):
+        staged through pinned host memory and copied without blocking on the
+        current stream, which later launches on that stream follow. torch's
+        pinned-memory pool keeps the staging buffer until the copy is done."""
+        dev = torch.device(device)
+        pinned = torch.from_numpy(self.host).pin_memory()
+        self.dev = torch.empty(pinned.shape, dtype=pinned.dtype, device=dev)
+        self.dev.copy_(pinned, non_blocking=True)
         return self
 
 
@@ -125,6 +130,18 @@ def _need(t: torch.Tensor, name: str, dtype, shape, device):
         raise ValueError(f"{name} must be on {device}, got {t.device}")
 
 
+def c_args(p: Plan, q: torch.Tensor, k_new: torch.Tensor, v_new: torch.Tensor, k_cache: torch.Tensor,
+           v_cache: torch.Tensor, page_ids: torch.Tensor, out: torch.Tensor, lse: Optional[torch.Tensor],
+           workspace: Optional[torch.Tensor], stream) -> tuple:
+    """The argument list of sangam_attn_forward for already checked tensors."""
+    ws_ptr = workspace.data_ptr() if workspace is not None else None
+    ws_len = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    return (p.host_ptr(), p.dev.data_ptr(), q.data_ptr(), k_new.data_ptr(), v_new.data_ptr(),
+            k_cache.data_ptr(), v_cache.data_ptr(), int(k_cache.shape[0]), page_ids.data_ptr(),
+            int(page_ids.numel()), out.data_ptr(), lse.data_ptr() if lse is not None else None, ws_ptr,
+            ws_len, stream.cuda_stream)
+
+
 def forward(p: Plan, q: torch.Tensor, k_new: torch.Tensor, v_new: torch.Tensor,
             k_cache: torch.Tensor, v_cache: torch.Tensor, page_ids: torch.Tensor,
             out: Optional[torch.Tensor] = None, lse: Optional[torch.Tensor] = None,
@@ -165,12 +182,8 @@ def forward(p: Plan, q: torch.Tensor, k_new: torch.Tensor, v_new: torch.Tensor,
     wsb = p.workspace_bytes
     if wsb > 0 and workspace is None:
         workspace = torch.empty((wsb,), dtype=torch.uint8, device=dev)
-    ws_ptr = workspace.data_ptr() if workspace is not None else None
-    ws_len = workspace.numel() * workspace.element_size() if workspace is not None else 0
     s = stream if stream is not None else torch.cuda.current_stream(dev)
-    args = (p.host_ptr(), p.dev.data_ptr(), q.data_ptr(), k_new.data_ptr(), v_new.data_ptr(),
-            k_cache.data_ptr(), v_cache.data_ptr(), page_ids.data_ptr(), out.data_ptr(),
-            lse.data_ptr() if lse is not None else None, ws_ptr, ws_len, s.cuda_stream)
+    args = c_args(p, q, k_new, v_new, k_cache, v_cache, page_ids, out, lse, workspace, s)
     if launch_events is None:
         check(lib.sangam_attn_forward(*args))
     else:

@@ -778,8 +778,9 @@ bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) ==
 
 static sangam_status forward_impl(const void* plan_host, const void* plan_dev, const void* q,
                                   const void* k_new, const void* v_new, void* k_cache, void* v_cache,
-                                  const int32_t* page_ids_dev, void* out, float* lse, void* workspace,
-                                  size_t workspace_bytes, void* stream_ptr, void* const* events) {
+                                  int64_t pool_pages, const int32_t* page_ids_dev, int64_t num_page_ids,
+                                  void* out, float* lse, void* workspace, size_t workspace_bytes,
+                                  void* stream_ptr, void* const* events) {
     clear_error();
     const PlanHeader* h = check_plan(plan_host);
     if (!h) {
@@ -795,6 +796,16 @@ static sangam_status forward_impl(const void* plan_host, const void* plan_dev, c
         (reinterpret_cast<uintptr_t>(page_ids_dev) & 3u) || (lse && (reinterpret_cast<uintptr_t>(lse) & 3u))) {
         set_error("tensors must be 16-byte aligned (page_ids and lse 4-byte aligned)");
         return SANGAM_ERR_ALIGN;
+    }
+    if (pool_pages < h->num_pool_pages) {
+        set_error("the plan addresses " + std::to_string(h->num_pool_pages) + " pool pages, the cache holds " +
+                  std::to_string(pool_pages));
+        return SANGAM_ERR_BUFFER;
+    }
+    if (num_page_ids < h->total_pages) {
+        set_error("the plan reads " + std::to_string(h->total_pages) + " page ids, page_ids_dev holds " +
+                  std::to_string(num_page_ids));
+        return SANGAM_ERR_BUFFER;
     }
     if (h->workspace_bytes > 0) {
         if (!workspace || workspace_bytes < size_t(h->workspace_bytes)) {
@@ -893,25 +904,25 @@ static sangam_status forward_impl(const void* plan_host, const void* plan_dev, c
 
 extern "C" sangam_status sangam_attn_forward(const void* plan_host, const void* plan_dev, const void* q,
                                              const void* k_new, const void* v_new, void* k_cache,
-                                             void* v_cache, const int32_t* page_ids_dev, void* out,
-                                             float* lse, void* workspace, size_t workspace_bytes,
-                                             void* stream) {
+                                             void* v_cache, int64_t pool_pages, const int32_t* page_ids_dev,
+                                             int64_t num_page_ids, void* out, float* lse, void* workspace,
+                                             size_t workspace_bytes, void* stream) {
     clear_error();
-    return forward_impl(plan_host, plan_dev, q, k_new, v_new, k_cache, v_cache, page_ids_dev, out, lse,
-                        workspace, workspace_bytes, stream, nullptr);
+    return forward_impl(plan_host, plan_dev, q, k_new, v_new, k_cache, v_cache, pool_pages, page_ids_dev,
+                        num_page_ids, out, lse, workspace, workspace_bytes, stream, nullptr);
 }
 
 extern "C" sangam_status sangam_attn_forward_timed(const void* plan_host, const void* plan_dev,
                                                    const void* q, const void* k_new, const void* v_new,
-                                                   void* k_cache, void* v_cache,
-                                                   const int32_t* page_ids_dev, void* out, float* lse,
-                                                   void* workspace, size_t workspace_bytes, void* stream,
-                                                   void* const* events) {
+                                                   void* k_cache, void* v_cache, int64_t pool_pages,
+                                                   const int32_t* page_ids_dev, int64_t num_page_ids,
+                                                   void* out, float* lse, void* workspace,
+                                                   size_t workspace_bytes, void* stream, void* const* events) {
     clear_error();
     if (!events) {
         set_error("events must not be NULL");
         return SANGAM_ERR_INVALID_ARG;
     }
-    return forward_impl(plan_host, plan_dev, q, k_new, v_new, k_cache, v_cache, page_ids_dev, out, lse,
-                        workspace, workspace_bytes, stream, events);
+    return forward_impl(plan_host, plan_dev, q, k_new, v_new, k_cache, v_cache, pool_pages, page_ids_dev,
+                        num_page_ids, out, lse, workspace, workspace_bytes, stream, events);
 }

@@ -54,11 +54,11 @@ def _plan():
                      sm_scale=wl.sm_scale, force_kv_splits=2)
 
 
-def _fwd(plan_host, plan_dev=4096, q=4096, kn=4096, vn=4096, kc=4096, vc=4096, pid=4096, out=4096,
-         lse=None, ws=None, wsb=0):
+def _fwd(plan_host, plan_dev=4096, q=4096, kn=4096, vn=4096, kc=4096, vc=4096, pool=1 << 30, pid=4096,
+         npid=1 << 30, out=4096, lse=None, ws=None, wsb=0):
     # fake device addresses: every check below fails before any HIP call
-    return _lib.lib.sangam_attn_forward(plan_host, plan_dev, q, kn, vn, kc, vc, pid, out, lse, ws,
-                                        wsb, None)
+    return _lib.lib.sangam_attn_forward(plan_host, plan_dev, q, kn, vn, kc, vc, pool, pid, npid, out, lse,
+                                        ws, wsb, None)
 
 
 def test_forward_rejects_bad_plan():
@@ -81,6 +81,15 @@ def test_forward_rejects_null_and_misaligned():
     assert _fwd(p.host_ptr(), ws=None, wsb=0) == -5
     assert _fwd(p.host_ptr(), ws=4096, wsb=ws - 1) == -5
     assert b"workspace" in _lib.lib.sangam_last_error()
+
+
+def test_forward_rejects_small_pool_and_page_table():
+    p = _plan()
+    ws = p.workspace_bytes
+    assert _fwd(p.host_ptr(), pool=p.num_pool_pages - 1, ws=4096, wsb=ws) == -5
+    assert b"pool pages" in _lib.lib.sangam_last_error()
+    assert _fwd(p.host_ptr(), npid=p.total_pages - 1, ws=4096, wsb=ws) == -5
+    assert b"page ids" in _lib.lib.sangam_last_error()
 
 
 def test_last_error_clears_on_success():

@@ -151,6 +151,39 @@ def test_brute_force_tiny(hq, hkv):
     assert np.abs(lse - ref_lse).max() <= 1e-14
 
 
+@pytest.mark.parametrize("hq,hkv", [(2, 2), (4, 2)])
+def test_brute_force_multi_row_blocks(hq, hkv):
+    # cached items with more than 32 query rows (a larger decode block, one
+    # starting at 0 below a cached tail, one ending at the context's end) next
+    # to a prefill: the fresh rows replace exactly their positions
+    wl = workloads.make_workload("bfm", 6, hq=hq, hkv=hkv, d=4,
+                                 decodes=[(3, 40, 34), (0, 37, 33), (2, 38, 36)], prefills=[3])
+    assert [wl.n(i) for i in range(3)] == [34, 33, 36]
+    out, lse = oracle.attention_all(wl)
+    ref_out, ref_lse = brute_force(wl)
+    assert np.abs(out - ref_out).max() <= 1e-14
+    assert np.abs(lse - ref_lse).max() <= 1e-14
+    for i in range(3):
+        k, v = oracle.expected_kv(wl, i)
+        rk, rv = brute_force_kv(wl, i)
+        assert np.array_equal(k, rk) and np.array_equal(v, rv), f"item {i}"
+
+
+@pytest.mark.parametrize("hq,hkv", [(28, 4), (8, 8)])
+def test_head_subset_call_equals_full_call(hq, hkv):
+    # the reduced call that draws only the chosen heads (each paired with its
+    # own KV head) returns, bit for bit, the full call's values for them
+    wl = workloads.make_workload("sub", 5, hq=hq, hkv=hkv, d=64, decodes=[(30, 200), (0, 45, 40)],
+                                 prefills=[70])
+    full, full_lse = oracle.attention_all(wl)
+    heads = [hq - 1, 0, hq // 2, 1]
+    res = oracle.attention(wl, heads=heads)
+    for i, (rr, o, l) in res.items():
+        base = int(wl.q_indptr[i])
+        assert np.array_equal(o, full[base + rr][:, heads]), f"item {i}"
+        assert np.array_equal(l, full_lse[base + rr][:, heads]), f"item {i}"
+
+
 def test_brute_force_scale():
     wl = workloads.make_workload("bf", 3, hq=2, hkv=1, d=4, decodes=[(1, 6)], prefills=[4],
                                  sm_scale=0.3)
@@ -263,7 +296,7 @@ def test_zero_query_gives_mean():
     del base_q
 
 
-def test_weights_sum_to_one_and_match_softmax():
+def test_weights_sum_to_one():
     wl = workloads.ragged_small(0, hq=4, hkv=2, d=64)
     rows = [0, 5, wl.total_q - 1, int(wl.q_indptr[3]) + 2]
     for r in rows:
@@ -271,6 +304,32 @@ def test_weights_sum_to_one_and_match_softmax():
             w = oracle.weights(wl, r, h)
             assert abs(w.sum() - 1.0) <= 1e-13
             assert (w >= 0).all()
+
+
+def test_weights_match_softmax_of_exact_scores():
+    # the debug entry's weights of every (packed row, head) against a softmax
+    # taken here of exact-rational scores over the item's own assembled
+    # sequence: a wrong row, head, KV group or position map shows
+    wl = workloads.make_workload("w", 9, hq=4, hkv=2, d=8, decodes=[(3, 11), (0, 6, 5)], prefills=[7],
+                                 pos_decodes=[([1, 6], 9)])
+    G = 2
+    sigma = Fraction(float(np.float32(wl.sm_scale)))
+    for i in range(wl.num_items):
+        q = wl.q(i).float().numpy()
+        kn = wl.k_new(i).float().numpy()
+        kc = wl.k_ctx(i)
+        row_at = {int(p): r for r, p in enumerate(wl.positions(i))}
+        L = int(wl.kv_len[i])
+        K = [kn[row_at[j]] if j in row_at else kc[j].float().numpy() for j in range(L)]
+        for r in range(wl.n(i)):
+            for h in range(4):
+                s = [sigma * sum(Fraction(float(q[r, h, e])) * Fraction(float(K[j][h // G, e])) for e in range(8))
+                     for j in range(L)]
+                m = max(s)
+                e = [math.exp(float(sj - m)) for sj in s]
+                Z = math.fsum(e)
+                w = oracle.weights(wl, int(wl.q_indptr[i]) + r, h)
+                assert np.abs(w - np.asarray(e) / Z).max() <= 1e-15, (i, r, h)
 
 
 # -------------------------------------------------------------- invariants

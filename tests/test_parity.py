@@ -201,26 +201,134 @@ def test_dream_mixed(dev, seed):
     check_pool_untouched(wl, t)
 
 
-def test_prefill_heavy(dev):
-    wl = workloads.prefill_heavy(0)
+def tile_rows(n, rng, tile=128):
+    """One random row from every `tile`-row block of an item, plus its first
+    and last rows."""
+    picks = [int(rng.integers(b, min(n, b + tile))) for b in range(0, n, tile)]
+    return np.unique(np.r_[0, n - 1, picks])
+
+
+def spread_heads(rng, hq, hkv, count):
+    """`count` query heads from distinct KV groups (as many as there are)."""
+    G = hq // hkv
+    groups = rng.permutation(hkv)[:count]
+    if len(groups) < count:
+        groups = np.r_[groups, rng.integers(0, hkv, count - len(groups))]
+    return sorted({int(g) * G + int(rng.integers(0, G)) for g in groups})
+
+
+def check_fresh_rows(wl, t, items):
+    """The fresh rows of each item sit bit-exact at their positions in the pages."""
+    for i in items:
+        pos = wl.positions(i)
+        pages = torch.from_numpy(wl.item_pages(i)[pos // 16].astype(np.int64)).to(t["k_cache"].device)
+        slots = torch.from_numpy((pos % 16).astype(np.int64)).to(t["k_cache"].device)
+        for pool, fresh in ((t["k_cache"], wl.k_new(i)), (t["v_cache"], wl.v_new(i))):
+            got = pool[pages, :, slots].cpu()  # [n, Hkv, D]
+            assert torch.equal(got.view(torch.int16), fresh.view(torch.int16)), f"item {i}: fresh rows"
+
+
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_prefill_heavy(dev, seed):
+    """Every 128-row tile of every prefill is sampled (one random row each,
+    plus the first and last row) on three query heads of distinct KV groups
+    per item; the cache of every item is compared bit for bit."""
+    wl = workloads.prefill_heavy(seed)
     p, t, out, lse = run(wl, dev)
-    rng = np.random.default_rng(5)
-    rows = {i: np.unique(np.r_[0, wl.n(i) - 1, rng.integers(0, wl.n(i), 10)]) for i in range(wl.num_items)}
-    check_sampled(wl, out, lse, items=list(range(wl.num_items)), rows_per_item=rows)
-    check_cache(wl, t, items=[0, wl.num_items - 1])
+    rng = np.random.default_rng(50 + seed)
+    for i in range(wl.num_items):
+        rows = {i: tile_rows(wl.n(i), rng)}
+        heads = spread_heads(rng, wl.num_q_heads, wl.num_kv_heads, 3)
+        check_sampled(wl, out, lse, items=[i], rows_per_item=rows, heads=heads)
+    check_cache(wl, t)
     check_pool_untouched(wl, t)
 
 
-def test_long_decode(dev):
-    wl = workloads.long_decode(0)
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_long_decode(dev, seed):
+    """All 256 block decodes, every row, on four query heads spread over the
+    KV heads (MHA: each its own group); the fresh rows of every item and the
+    whole cache of the split items and eight others bit for bit."""
+    wl = workloads.long_decode(seed)
     p, t, out, lse = run(wl, dev)
     order = np.argsort(-wl.kv_len)
-    rng = np.random.default_rng(7)
-    items = sorted(set(order[:6].tolist()) | set(rng.choice(wl.num_items, 10, replace=False).tolist()))
     assert int(wl.kv_len[order[0]]) > 8192  # split-KV path exercised
-    check_sampled(wl, out, lse, items=items, heads=[0, 13, 31])
-    check_cache(wl, t, items=items)
+    heads = [seed, 9 + seed, 18 + seed, 31 - seed]
+    check_sampled(wl, out, lse, items=list(range(wl.num_items)), heads=heads)
+    check_fresh_rows(wl, t, range(wl.num_items))
+    rng = np.random.default_rng(70 + seed)
+    split = [i for i in range(wl.num_items) if len(p.item_splits(i)) > 2]
+    assert split
+    full = sorted(set(split) | set(rng.choice(wl.num_items, 8, replace=False).tolist()))
+    check_cache(wl, t, items=full)
     check_pool_untouched(wl, t)
+
+
+# cached items with more than 32 rows (larger decode blocks): the rows run in
+# prefill-shaped tiles over paged context; (o, L, n) with unaligned offsets, a
+# block from position 0 under a cached tail, tiles spanning several 128-row
+# blocks, and contexts past the 8192-key range limit whose split boundary a
+# block straddles (L = 9000: chunks of 4544 keys)
+CACHED_BLOCKS = [(100, 500, 64), (37, 300, 33), (0, 2000, 300), (1500, 9000, 200), (4500, 9000, 100),
+                 (8190, 8400, 150)]
+
+
+@pytest.mark.parametrize("hq,hkv,d", [(32, 32, 128), (28, 4, 128), (8, 2, 64)])
+@pytest.mark.parametrize("with_decodes", [False, True])
+@pytest.mark.parametrize("force", [0, 3])
+def test_cached_multi_row_blocks(dev, hq, hkv, d, with_decodes, force):
+    decodes = list(CACHED_BLOCKS) + ([(20, 700), (300, 333)] if with_decodes else [])
+    wl = workloads.make_workload("cached_blocks", 31, hq=hq, hkv=hkv, d=d, decodes=decodes,
+                                 prefills=[150] if with_decodes else [])
+    p, t, out, lse = run(wl, dev, force_splits=force)
+    assert p.info.num_prefill_tiles > 0
+    check_full(wl, out, lse)
+    check_cache(wl, t)
+    check_pool_untouched(wl, t)
+
+
+def test_sequential_prefill_then_decode(dev):
+    """The cached-dLLM cycle in two calls (the single-request workload's
+    sequential reading): a prefill call writes the request's pages, then a
+    block decode call over those same pages reads them as its cache and
+    refreshes rows 96..127. The decode matches the oracle (whose cache is the
+    prefill's K/V) and the prefill's own rows 96..127."""
+    from paper_2607_04206_amd import attn
+    base = workloads.tiny_mixed(0)
+    pre = workloads.make_workload("seq_prefill", 0, hq=4, hkv=4, d=64, decodes=[], prefills=[128])
+    dec = workloads.make_workload("seq_decode", 0, hq=4, hkv=4, d=64, decodes=[(96, 128)], prefills=[])
+    dec.page_ids = pre.page_ids.copy()
+    dec.num_pool_pages = pre.num_pool_pages
+
+    def pre_vals(item, kind):  # the prefill draws as the single-request workload's item 1
+        return {workloads.KIND_Q: base.q(1), workloads.KIND_KNEW: base.k_new(1),
+                workloads.KIND_VNEW: base.v_new(1)}[kind].float()
+
+    def dec_vals(item, kind):  # the decode as its item 0 (cache = the prefill's K/V)
+        return {workloads.KIND_Q: base.q(0), workloads.KIND_KNEW: base.k_new(0), workloads.KIND_VNEW: base.v_new(0),
+                workloads.KIND_KCTX: base.k_ctx(0), workloads.KIND_VCTX: base.v_ctx(0)}[kind].float()
+
+    pre.value_fn, dec.value_fn = pre_vals, dec_vals
+    t = workloads.device_inputs(pre, dev)  # NaN pool: the decode reads only what the prefill wrote
+    p1 = attn.plan(q_indptr=pre.q_indptr, q_offset=pre.q_offset, kv_len=pre.kv_len,
+                   page_indptr=pre.page_indptr, page_ids=pre.page_ids, num_q_heads=4, num_kv_heads=4,
+                   head_dim=64, num_pool_pages=pre.num_pool_pages, sm_scale=pre.sm_scale, device=dev)
+    out1, lse1 = attn.forward(p1, t["q"], t["k_new"], t["v_new"], t["k_cache"], t["v_cache"], t["page_ids"])
+    p2 = attn.plan(q_indptr=dec.q_indptr, q_offset=dec.q_offset, kv_len=dec.kv_len,
+                   page_indptr=dec.page_indptr, page_ids=dec.page_ids, num_q_heads=4, num_kv_heads=4,
+                   head_dim=64, num_pool_pages=dec.num_pool_pages, sm_scale=dec.sm_scale, device=dev)
+    out2, lse2 = attn.forward(p2, dec.packed_q(dev), dec.packed_k_new(dev), dec.packed_v_new(dev),
+                              t["k_cache"], t["v_cache"], t["page_ids"])
+    torch.cuda.synchronize()
+    check_full(pre, out1, lse1)
+    check_full(dec, out2, lse2)
+    check_cache(dec, t)
+    check_pool_untouched(pre, t)
+    # the decode's rows are the prefill's rows 96..127
+    assert (out2.float() - out1[96:128].float()).abs().max().item() <= 1e-2
+    # and the one-call reading (decode and prefill side by side on disjoint pages) agrees
+    _, _, out_one, _ = run(base, dev)
+    assert (out2.float() - out_one[:32].float()).abs().max().item() <= 1e-2
 
 
 @pytest.mark.parametrize("hq,hkv,with_prefill,cus", [(8, 8, False, 0), (28, 4, False, 0), (28, 4, False, 8),

@@ -106,6 +106,10 @@ def coverage(wl, p):
     lambda: workloads.make_workload("g2", 4, hq=8, hkv=4, d=64, decodes=[(32, 700)], prefills=[100]),
     lambda: workloads.token_cache_decodes(2, hq=8, hkv=8, d=64, count=5),
     lambda: workloads.token_cache_decodes(3, hq=28, hkv=4, d=128, count=4, prefills=[150]),
+    lambda: workloads.make_workload("mb", 5, hq=28, hkv=4, d=128, prefills=[150],
+                                    decodes=[(100, 500, 64), (37, 300, 33), (1500, 9000, 200), (20, 700)]),
+    lambda: workloads.make_workload("mbm", 6, hq=8, hkv=8, d=64, prefills=[],
+                                    decodes=[(0, 2000, 300), (4500, 9000, 100), (8190, 8400, 150)]),
 ])
 @pytest.mark.parametrize("force", [0, 1, 3, 8])
 def test_every_row_head_key_covered_once(mk, force):
@@ -431,3 +435,21 @@ def test_position_list_validation(pos, L, msg):
         attn.plan(q_indptr=q_indptr, q_offset=np.zeros(len(kv_len), np.int32), kv_len=kv_len,
                   page_indptr=page_indptr, page_ids=page_ids, num_q_heads=2, num_kv_heads=2,
                   head_dim=64, num_pool_pages=4096, sm_scale=0.125, q_pos=q_pos)
+
+
+@pytest.mark.parametrize("hq,hkv", [(28, 4), (32, 32)])
+def test_cached_multi_row_blocks_plan(hq, hkv):
+    """A cached item with more than 32 rows (a larger decode block) runs in
+    prefill-shaped tiles of 128 rows over its paged context; a context longer
+    than the cached-range limit is cut into ranges of at most 8192 keys."""
+    wl = workloads.make_workload("mb", 3, hq=hq, hkv=hkv, d=128, prefills=[],
+                                 decodes=[(100, 500, 64), (1500, 9000, 200), (8190, 8400, 150)])
+    h, items, dec, pre, mer = parse(plan_of(wl))
+    assert len(dec) == 0
+    assert [int(x) for x in items["num_splits"]] == [1, 2, 2]
+    for t in pre:
+        assert t["flags"] == 0 and t["kv_end"] - t["kv_begin"] <= 8192
+    per_item = np.bincount(pre["item"], minlength=3)
+    # item 0: 1 row block, items 1 and 2: 2 row blocks of 128, each split in two
+    assert list(per_item) == [hq, 2 * 2 * hq, 2 * 2 * hq]
+    assert len(mer) == 200 + 150

@@ -1,6 +1,7 @@
 """Deficit token-budget admission (Sec. 4.1, Alg. 1): the library's native
 rule against the paper's worked example, the guarantees the paper states for
-it, and a plain transcription of the algorithm (oracle/deficit.py)."""
+it, and a closed-form restatement of the rule (oracle/deficit.py: the longest
+head of the queue whose prefix sum fits the budget)."""
 import ctypes
 import os
 
@@ -70,9 +71,23 @@ def random_stream(seed, T=400, tau=1024, max_decodes=40, min_decodes=0):
 
 
 @pytest.mark.parametrize("seed", range(6))
-def test_library_matches_transcription(seed):
+def test_library_matches_closed_form(seed):
     tau, decs, arr = random_stream(seed)
     assert simulate(admit, tau, decs, arr) == simulate(ref.admit, tau, decs, arr)
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_library_matches_closed_form_single_iterations(seed):
+    # single iterations over a wide range: budgets below zero (decodes over
+    # tau), idle microbatches, oversized heads, carries larger than tau
+    rng = np.random.default_rng(100 + seed)
+    for _ in range(2000):
+        tau = int(rng.integers(0, 4096))
+        dec = [32] * int(rng.integers(0, 80))
+        waiting = [int(x) for x in rng.integers(1, 5000, size=int(rng.integers(0, 6)))]
+        deficit = int(rng.integers(0, 6000))
+        assert admit(tau, dec, waiting, deficit) == ref.admit(tau, dec, waiting, deficit), \
+            (tau, len(dec), waiting, deficit)
 
 
 @pytest.mark.parametrize("seed", range(6))

@@ -35,6 +35,7 @@ from __future__ import annotations
 
 import dataclasses
 import math
+import os
 from typing import Callable, List, Optional, Sequence, Tuple
 
 import numpy as np
@@ -91,39 +92,48 @@ class Workload:
         return np.arange(int(self.q_offset[i]), int(self.q_offset[i]) + self.n(i), dtype=np.int64)
 
     # ------------------------------------------------------------------ values
-    def _draw(self, item: int, kind: int, shape: Tuple[int, ...], device="cpu") -> torch.Tensor:
+    def _draw(self, item: int, kind: int, shape: Tuple[int, ...], device="cpu",
+              heads: Optional[Sequence[int]] = None) -> torch.Tensor:
+        """Piece (item, kind) of shape [rows, H, D]; with ``heads``, only those
+        entries of axis 1 ([rows, len(heads), D]), drawn without the others."""
         if self.value_fn is not None:
             t = self.value_fn(item, kind)
             if t is not None:
                 assert tuple(t.shape) == tuple(shape), (t.shape, shape)
+                if heads is not None:
+                    t = t[:, list(heads)]
                 return t.to(torch.bfloat16).to(device)
         scale = self.q_scale if kind == KIND_Q else 1.0
-        return counter_normal_bf16(self.seed, item, kind, shape, device=device, scale=scale)
+        if heads is None:
+            return counter_normal_bf16(self.seed, item, kind, shape, device=device, scale=scale)
+        return counter_normal_bf16_heads(self.seed, item, kind, shape, heads, device=device, scale=scale)
 
-    def q(self, i: int, device="cpu") -> torch.Tensor:
-        """Query rows of item i, bf16 [n_i, Hq, D]."""
-        return self._draw(i, KIND_Q, (self.n(i), self.num_q_heads, self.head_dim), device)
+    def q(self, i: int, device="cpu", heads=None) -> torch.Tensor:
+        """Query rows of item i, bf16 [n_i, Hq, D] (or only the listed heads)."""
+        return self._draw(i, KIND_Q, (self.n(i), self.num_q_heads, self.head_dim), device, heads)
 
-    def k_new(self, i: int, device="cpu") -> torch.Tensor:
+    def k_new(self, i: int, device="cpu", heads=None) -> torch.Tensor:
         """Fresh keys of item i (positions o_i .. o_i+n_i-1), bf16 [n_i, Hkv, D]."""
-        return self._draw(i, KIND_KNEW, (self.n(i), self.num_kv_heads, self.head_dim), device)
+        return self._draw(i, KIND_KNEW, (self.n(i), self.num_kv_heads, self.head_dim), device, heads)
 
-    def v_new(self, i: int, device="cpu") -> torch.Tensor:
-        return self._draw(i, KIND_VNEW, (self.n(i), self.num_kv_heads, self.head_dim), device)
+    def v_new(self, i: int, device="cpu", heads=None) -> torch.Tensor:
+        return self._draw(i, KIND_VNEW, (self.n(i), self.num_kv_heads, self.head_dim), device, heads)
 
-    def k_ctx(self, i: int, device="cpu") -> Optional[torch.Tensor]:
+    def k_ctx(self, i: int, device="cpu", heads=None) -> Optional[torch.Tensor]:
         """Cache content before the call for positions [0, L_i), bf16 [L_i, Hkv, D].
 
         None for a prefill (it brings its whole sequence as fresh rows). Rows
         [o_i, o_i+n_i) hold stale values that the call must overwrite."""
         if self.is_prefill[i]:
             return None
-        return self._draw(i, KIND_KCTX, (int(self.kv_len[i]), self.num_kv_heads, self.head_dim), device)
+        return self._draw(i, KIND_KCTX, (int(self.kv_len[i]), self.num_kv_heads, self.head_dim), device,
+                          heads)
 
-    def v_ctx(self, i: int, device="cpu") -> Optional[torch.Tensor]:
+    def v_ctx(self, i: int, device="cpu", heads=None) -> Optional[torch.Tensor]:
         if self.is_prefill[i]:
             return None
-        return self._draw(i, KIND_VCTX, (int(self.kv_len[i]), self.num_kv_heads, self.head_dim), device)
+        return self._draw(i, KIND_VCTX, (int(self.kv_len[i]), self.num_kv_heads, self.head_dim), device,
+                          heads)
 
     # ------------------------------------------------------- packed views
     def packed_q(self, device="cpu") -> torch.Tensor:
@@ -200,6 +210,49 @@ def _lowbias32(x: torch.Tensor) -> torch.Tensor:
     return x ^ (x >> 16)
 
 
+def _hash_u32_np(idx: np.ndarray, key: int) -> np.ndarray:
+    """The same element hash as the torch path, on uint32 numpy arrays, whose
+    multiplications wrap modulo 2^32 by themselves (host draws)."""
+    with np.errstate(over="ignore"):
+        x = idx.astype(np.uint32, copy=True)
+        x *= np.uint32(0x27D4EB2F)
+        x += np.uint32(key)
+        x ^= x >> np.uint32(16)
+        x *= np.uint32(0x7FEB352D)
+        x ^= x >> np.uint32(15)
+        x *= np.uint32(0x846CA68B)
+        x ^= x >> np.uint32(16)
+    return x
+
+
+_HOST_POOL = None
+_HOST_CHUNK = 1 << 18
+
+
+def _draw_host(key: int, idx: np.ndarray, table: torch.Tensor) -> torch.Tensor:
+    """Table entries at the hashed indices, drawn in parallel pieces (numpy
+    releases the interpreter lock in its element loops)."""
+    global _HOST_POOL
+    bits = table.view(torch.int16).numpy()
+    out = np.empty(idx.shape[0], np.int16)
+
+    def piece(a, b):
+        h = _hash_u32_np(idx[a:b], key)
+        h >>= np.uint32(8)
+        h &= np.uint32(0xFFFF)
+        np.take(bits, h, out=out[a:b])
+
+    n = idx.shape[0]
+    if n <= _HOST_CHUNK:
+        piece(0, n)
+    else:
+        if _HOST_POOL is None:
+            from concurrent.futures import ThreadPoolExecutor
+            _HOST_POOL = ThreadPoolExecutor(max_workers=min(16, len(os.sched_getaffinity(0))))
+        list(_HOST_POOL.map(lambda a: piece(a, min(n, a + _HOST_CHUNK)), range(0, n, _HOST_CHUNK)))
+    return torch.from_numpy(out).view(torch.bfloat16)
+
+
 def normal_table(device="cpu", scale: float = 1.0) -> torch.Tensor:
     """65536 bf16 quantiles of N(0, 1) (times scale, before rounding)."""
     key = (str(device), float(scale))
@@ -226,12 +279,47 @@ def counter_normal_bf16(seed: int, item: int, kind: int, shape, device="cpu", sc
     key = piece_key(seed, item, kind)
     table = normal_table(device, scale)
     out = torch.empty(n, dtype=torch.bfloat16, device=device)
+    host = torch.device(device).type == "cpu"
     for c0 in range(0, n, chunk):
         c1 = min(n, c0 + chunk)
+        if host:
+            out[c0:c1] = _draw_host(key, np.arange(c0, c1, dtype=np.uint32), table)
+            continue
         idx = torch.arange(c0, c1, dtype=torch.int64, device=device)
         h = _lowbias32((_mul32(idx, 0x27D4EB2F) + key) & _M32)
         out[c0:c1] = table[(h >> 8) & 0xFFFF]
     return out.view(*shape)
+
+
+def counter_normal_bf16_heads(seed: int, item: int, kind: int, shape, heads: Sequence[int], device="cpu",
+                              scale: float = 1.0, chunk: int = 1 << 24) -> torch.Tensor:
+    """The entries [:, heads, :] of piece (seed, item, kind) of shape [rows, H,
+    D], drawn from their own counters (c = (row * H + h) * D + d) without the
+    other heads: bitwise the same values as slicing the whole piece."""
+    rows, H, D = (int(x) for x in shape)
+    hs = torch.as_tensor(list(heads), dtype=torch.int64, device=device)
+    if hs.numel() and (int(hs.min()) < 0 or int(hs.max()) >= H):
+        raise IndexError("head out of range")
+    if rows * H * D >= (1 << 32):
+        raise ValueError("a piece must have fewer than 2^32 elements")
+    key = piece_key(seed, item, kind)
+    table = normal_table(device, scale)
+    per_row = hs.numel() * D
+    out = torch.empty(rows * per_row, dtype=torch.bfloat16, device=device)
+    inner = (hs[:, None] * D + torch.arange(D, dtype=torch.int64, device=device)[None, :]).reshape(-1)
+    step = max(1, chunk // max(per_row, 1))
+    host = torch.device(device).type == "cpu"
+    inner_np = inner.cpu().numpy().astype(np.uint32) if host else None
+    for r0 in range(0, rows, step):
+        r1 = min(rows, r0 + step)
+        if host:
+            idx_np = (np.arange(r0, r1, dtype=np.uint32)[:, None] * np.uint32(H * D) + inner_np[None, :]).reshape(-1)
+            out[r0 * per_row:r1 * per_row] = _draw_host(key, idx_np, table)
+            continue
+        idx = (torch.arange(r0, r1, dtype=torch.int64, device=device)[:, None] * (H * D) + inner[None, :]).reshape(-1)
+        h = _lowbias32((_mul32(idx, 0x27D4EB2F) + key) & _M32)
+        out[r0 * per_row:r1 * per_row] = table[(h >> 8) & 0xFFFF]
+    return out.view(rows, hs.numel(), D)
 
 # ---------------------------------------------------------------- builders
 def _lognormal_lengths(rng, count, median, sigma, lo, hi) -> np.ndarray:
@@ -245,17 +333,22 @@ def make_workload(name: str, seed: int, *, hq: int, hkv: int, d: int,
                   q_scale: float = 1.0, page_size: int = PAGE_SIZE,
                   sm_scale: Optional[float] = None,
                   pos_decodes: Sequence[Tuple[Sequence[int], int]] = ()) -> Workload:
-    """decodes: list of (o, L) for 32-row block decodes (n = min(32, L - o));
+    """decodes: list of (o, L) for 32-row block decodes (n = min(32, L - o)),
+    or (o, L, n) for a block of n rows at positions o .. o+n-1 over a cached
+    context (n may exceed 32: a larger decode block);
     pos_decodes: list of (positions, L) for decodes that recompute the given
     strictly increasing positions (placed after the block decodes);
     prefills: list of L. Pages are drawn from ``rng`` (default: seeded by seed)."""
     if rng is None:
         rng = np.random.default_rng(seed)
     q_off, kv_len, n_rows, pre, pos = [], [], [], [], []
-    for (o, L) in decodes:
+    for dec in decodes:
+        o, L = dec[0], dec[1]
+        n = dec[2] if len(dec) > 2 else min(BLOCK, L - o)
+        assert 1 <= n and o >= 0 and o + n <= L, dec
         q_off.append(o)
         kv_len.append(L)
-        n_rows.append(min(BLOCK, L - o))
+        n_rows.append(n)
         pre.append(False)
         pos.append(np.arange(o, o + n_rows[-1]))
     for (pp, L) in pos_decodes:
