@@ -159,6 +159,33 @@ sangam_status sangam_attn_forward(const void *plan_host, const void *plan_dev, c
                                   size_t workspace_bytes, void *stream);
 
 /*
+ * For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation): the same
+ * call as sangam_attn_forward, with the split-KV partial results in a
+ * library-owned device array instead of a caller workspace. It calls no
+ * allocator. The array holds sangam_noalloc_scratch_bytes() bytes (32 MiB)
+ * per GPU; each GPU the library runs on keeps its own copy until the process
+ * ends. Its address is looked up once per device, on the first call with
+ * that device current. `stream` must belong to the current device.
+ * Every call on one GPU shares that GPU's array: two calls that overlap in
+ * time on one GPU (different streams, or threads) race on it; serialize
+ * them. The array keeps the last call's contents; nothing in it needs to
+ * start at zero (each split's partials are written before they are read).
+ * Errors: as sangam_attn_forward; SANGAM_ERR_BUFFER when the plan's
+ * workspace (sangam_plan_workspace_bytes) exceeds the array;
+ * SANGAM_ERR_INVALID_ARG when `stream` belongs to another device.
+ */
+sangam_status sangam_attn_forward_noalloc(const void *plan_host, const void *plan_dev, const void *q,
+                                          const void *k_new, const void *v_new, void *k_cache,
+                                          void *v_cache, int64_t pool_pages,
+                                          const int32_t *page_ids_dev, int64_t num_page_ids,
+                                          void *out, float *lse, void *stream);
+
+/* Bytes of the device array that sangam_attn_forward_noalloc uses for split
+ * partials (its largest plan workspace). */
+size_t sangam_noalloc_scratch_bytes(void);
+
+/*
  * sangam_attn_forward, plus HIP events carried by its launches, for measuring
  * each kernel in place: events[0] and [1] are the start and stop of the
  * prefill-shaped attention launch, [2] and [3] of the decode-shaped launch,

@@ -36,6 +36,8 @@ EXPORTS = (
     "sangam_plan_item_splits",
     "sangam_attn_forward",
     "sangam_attn_forward_timed",
+    "sangam_attn_forward_noalloc",
+    "sangam_noalloc_scratch_bytes",
     "sangam_last_error",
     "sangam_version",
     "sangam_deficit_admit",
@@ -126,6 +128,10 @@ def _load():
     lib.sangam_attn_forward.restype = ctypes.c_int32
     lib.sangam_attn_forward_timed.argtypes = [P, P, P, P, P, P, P, I64, P, I64, P, P, P, S, P, P]
     lib.sangam_attn_forward_timed.restype = ctypes.c_int32
+    lib.sangam_attn_forward_noalloc.argtypes = [P, P, P, P, P, P, P, I64, P, I64, P, P, P]
+    lib.sangam_attn_forward_noalloc.restype = ctypes.c_int32
+    lib.sangam_noalloc_scratch_bytes.argtypes = []
+    lib.sangam_noalloc_scratch_bytes.restype = S
     lib.sangam_kv_plan.argtypes = [ctypes.POINTER(KvDesc), P, S, ctypes.POINTER(S)]
     lib.sangam_kv_plan.restype = ctypes.c_int32
     lib.sangam_kv_plan_rows.argtypes = [P]

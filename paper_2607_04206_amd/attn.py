@@ -192,3 +192,33 @@ def forward(p: Plan, q: torch.Tensor, k_new: torch.Tensor, v_new: torch.Tensor,
         evs = (ctypes.c_void_p * 6)(*[e.cuda_event for e in launch_events])
         check(lib.sangam_attn_forward_timed(*args, evs))
     return out, lse
+
+
+def forward_noalloc(p: Plan, q: torch.Tensor, k_new: torch.Tensor, v_new: torch.Tensor,
+                    k_cache: torch.Tensor, v_cache: torch.Tensor, page_ids: torch.Tensor,
+                    out: torch.Tensor, lse: Optional[torch.Tensor] = None,
+                    stream: Optional[torch.cuda.Stream] = None) -> Tuple[torch.Tensor, Optional[torch.Tensor]]:
+    """sangam_attn_forward_noalloc: the forward with split partials in the
+    library's own device array, for callers that cannot allocate. out (and
+    lse, when wanted) are the caller's; the plan must already be on the
+    device (Plan.to) and its workspace within sangam_noalloc_scratch_bytes()."""
+    dev = q.device
+    T, Hq, Hkv, D = p.total_q, p.num_q_heads, p.num_kv_heads, p.head_dim
+    _need(q, "q", torch.bfloat16, (T, Hq, D), dev)
+    _need(k_new, "k_new", torch.bfloat16, (T, Hkv, D), dev)
+    _need(v_new, "v_new", torch.bfloat16, (T, Hkv, D), dev)
+    _need(k_cache, "k_cache", torch.bfloat16, None, dev)
+    _need(v_cache, "v_cache", torch.bfloat16, tuple(k_cache.shape), dev)
+    if k_cache.dim() != 4 or k_cache.shape[1] != Hkv or k_cache.shape[2] != 16 or k_cache.shape[3] != D:
+        raise ValueError("k_cache must be [num_pool_pages, Hkv, 16, D]")
+    _need(page_ids, "page_ids", torch.int32, None, dev)
+    _need(out, "out", torch.bfloat16, (T, Hq, D), dev)
+    if lse is not None:
+        _need(lse, "lse", torch.float32, (T, Hq), dev)
+    if p.dev is None or p.dev.device != dev:
+        raise ValueError("the plan is not on the device: call Plan.to(device) first")
+    s = stream if stream is not None else torch.cuda.current_stream(dev)
+    args = c_args(p, q, k_new, v_new, k_cache, v_cache, page_ids, out, lse, None, s)
+    # the same arguments without the workspace pointer and size
+    check(lib.sangam_attn_forward_noalloc(*args[:12], args[14]))
+    return out, lse

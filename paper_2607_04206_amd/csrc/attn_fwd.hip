@@ -26,6 +26,7 @@
 #include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
+#include <mutex>
 #include <string>
 
 #include "../../include/sangam_attn.h"
@@ -776,11 +777,55 @@ bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) ==
 
 }  // namespace
 
+// ---------------------------------------------------------- allocation-free
+// Split-KV partial results of sangam_attn_forward_noalloc live in this array
+// instead of a caller workspace. Each GPU the library runs on holds its own
+// copy for the life of the process. In host code the name is only a stand-in
+// for the symbol: kernels receive the device address that hipGetSymbolAddress
+// returns for the current device, cached per device below.
+namespace {
+constexpr size_t kScratchBytes = size_t(32) << 20;
+static __device__ __align__(256) uint8_t scratch[kScratchBytes];
+
+constexpr int kMaxScratchDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_dev[kMaxScratchDevices] = {};
+
+// the scratch array's address on the device that runs `stream`, which must
+// be the current device (the symbol is resolved with that device current)
+sangam_status scratch_address(hipStream_t stream, void** addr) {
+    int cur = -1;
+    if (hipError_t e = hipGetDevice(&cur); e != hipSuccess) return hip_fail(e, "hipGetDevice");
+    if (stream) {
+        hipDevice_t sd = -1;
+        if (hipError_t e = hipStreamGetDevice(stream, &sd); e != hipSuccess) return hip_fail(e, "hipStreamGetDevice");
+        if (int(sd) != cur) {
+            set_error("the stream belongs to device " + std::to_string(int(sd)) + ", the current device is " +
+                      std::to_string(cur));
+            return SANGAM_ERR_INVALID_ARG;
+        }
+    }
+    if (cur < 0 || cur >= kMaxScratchDevices) {
+        set_error("device ordinal " + std::to_string(cur) + " beyond the scratch table");
+        return SANGAM_ERR_UNSUPPORTED;
+    }
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_dev[cur]) {
+        void* p = nullptr;
+        if (hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)); e != hipSuccess)
+            return hip_fail(e, "hipGetSymbolAddress(scratch)");
+        g_scratch_dev[cur] = p;
+    }
+    *addr = g_scratch_dev[cur];
+    return SANGAM_OK;
+}
+}  // namespace
+
 static sangam_status forward_impl(const void* plan_host, const void* plan_dev, const void* q,
                                   const void* k_new, const void* v_new, void* k_cache, void* v_cache,
                                   int64_t pool_pages, const int32_t* page_ids_dev, int64_t num_page_ids,
                                   void* out, float* lse, void* workspace, size_t workspace_bytes,
-                                  void* stream_ptr, void* const* events) {
+                                  void* stream_ptr, void* const* events, bool use_scratch = false) {
     clear_error();
     const PlanHeader* h = check_plan(plan_host);
     if (!h) {
@@ -806,6 +851,17 @@ static sangam_status forward_impl(const void* plan_host, const void* plan_dev, c
         set_error("the plan reads " + std::to_string(h->total_pages) + " page ids, page_ids_dev holds " +
                   std::to_string(num_page_ids));
         return SANGAM_ERR_BUFFER;
+    }
+    if (use_scratch && h->workspace_bytes > 0) {
+        // the allocation-free entry point: split partials go to the scratch array
+        if (size_t(h->workspace_bytes) > kScratchBytes) {
+            set_error("the plan's split partials need " + std::to_string(h->workspace_bytes) +
+                      " bytes; the allocation-free forward holds " + std::to_string(kScratchBytes));
+            return SANGAM_ERR_BUFFER;
+        }
+        if (sangam_status st = scratch_address(static_cast<hipStream_t>(stream_ptr), &workspace); st != SANGAM_OK)
+            return st;
+        workspace_bytes = kScratchBytes;
     }
     if (h->workspace_bytes > 0) {
         if (!workspace || workspace_bytes < size_t(h->workspace_bytes)) {
@@ -910,6 +966,18 @@ extern "C" sangam_status sangam_attn_forward(const void* plan_host, const void* 
     clear_error();
     return forward_impl(plan_host, plan_dev, q, k_new, v_new, k_cache, v_cache, pool_pages, page_ids_dev,
                         num_page_ids, out, lse, workspace, workspace_bytes, stream, nullptr);
+}
+
+extern "C" size_t sangam_noalloc_scratch_bytes(void) { return kScratchBytes; }
+
+extern "C" sangam_status sangam_attn_forward_noalloc(const void* plan_host, const void* plan_dev, const void* q,
+                                                     const void* k_new, const void* v_new, void* k_cache,
+                                                     void* v_cache, int64_t pool_pages,
+                                                     const int32_t* page_ids_dev, int64_t num_page_ids,
+                                                     void* out, float* lse, void* stream) {
+    clear_error();
+    return forward_impl(plan_host, plan_dev, q, k_new, v_new, k_cache, v_cache, pool_pages, page_ids_dev,
+                        num_page_ids, out, lse, nullptr, 0, stream, nullptr, true);
 }
 
 extern "C" sangam_status sangam_attn_forward_timed(const void* plan_host, const void* plan_dev,
