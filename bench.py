@@ -4,15 +4,25 @@
 A step is one whole call: the prefill-shaped and the decode-shaped attention
 launches (which also write the fresh K/V rows back into their pages) and the
 split merge, over one batch whose inputs are already resident in HBM. Prints
-one JSON line (rank 0).
+one JSON line.
 
     python bench.py [--steps K] [--warmup W] [--workload NAME] [--seed S]
 
-Timing: a short untimed pass times each of the three launches with events
-carried in its dispatch (the phase breakdown); the timed region then runs K
-whole steps with events only on the dominant attention launch, whose average
-duration gives the roofline figure. ms_per_step is host wall time over the K
-steps, bracketed by device synchronisation.
+Protocol:
+- the plan is timed on the host (median of 5);
+- W warm-up steps;
+- a per-launch breakdown (events in each launch's dispatch; null for a
+  launch that has no work);
+- the timed region: K steps back to back, bracketed by device
+  synchronisation, with events only on the dominant attention launch;
+  ms_per_step is host wall time over those K steps, and the roofline figure
+  is that launch's mean duration (median and min beside it);
+- R flushed steps (--flushed-reps): before each, a 1 GiB read outside the
+  timing evicts the previous step's data from the 256 MB Infinity Cache; the
+  step and the dominant launch are timed with events (median and min);
+- the chip's measured ceilings (a 4 GiB streaming read, an MFMA-only loop),
+  against which the fractions are reported beside the spec-sheet peaks;
+- the oracle on a bounded CPU sample (median of 3 after a warm-up).
 
 Work counts are algorithmic: F = sum 4 n L D Hq flops (QK^T and PV, no causal
 halving) and B = K/V read once per item + cache write of the fresh rows + Q
@@ -55,68 +65,117 @@ def split_work(wl, fused_decodes=False):
     }
 
 
-def cpu_baseline(wl, budget_s):
-    """Time the oracle (as it stands) on a bounded sample of the same workload:
-    every block decode, then evenly spaced rows of each prefill, sized so the
-    oracle's own compute takes about budget_s. Input drawing is not timed."""
+def cpu_model():
+    """The host CPU's model name (lscpu, else /proc/cpuinfo)."""
+    import subprocess
+    try:
+        out = subprocess.run(["lscpu"], capture_output=True, text=True, timeout=10).stdout
+        for line in out.splitlines():
+            if line.startswith("Model name:"):
+                return line.split(":", 1)[1].strip()
+    except (OSError, subprocess.SubprocessError):
+        pass
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown CPU"
+
+
+def _oracle_sample(wl, target_flops, row_flops):
+    """Rows of a bounded sample: whole block decodes first, then evenly spaced
+    rows of each prefill, up to about target_flops."""
     import numpy as np
-    from oracle import oracle
-    threads = oracle.threads(len(os.sched_getaffinity(0)))
-    D, Hq = wl.head_dim, wl.num_q_heads
     dec = [i for i in range(wl.num_items) if wl.n(i) <= 32]
     pre = [i for i in range(wl.num_items) if wl.n(i) > 32]
-
-    def row_flops(i):
-        return 4.0 * int(wl.kv_len[i]) * D * Hq
-
-    # calibrate the oracle's rate on a piece of the workload large enough to
-    # keep every thread busy (a few whole block decodes, or 64 prefill rows)
-    cal_items = dec[:4] if dec else pre[:1]
-    cal_rows = {i: np.arange(wl.n(i) if wl.n(i) <= 32 else min(wl.n(i), 64)) for i in cal_items}
-    call = oracle.Call(wl, sorted(cal_rows))
-    sel, _, _ = oracle.selection(call, cal_rows)
-    t = time.perf_counter()
-    oracle.run(call, sel)
-    cal_flops = sum(len(r) * row_flops(i) for i, r in cal_rows.items())
-    rate = cal_flops / max(time.perf_counter() - t, 1e-6)
-    target = rate * budget_s
-
     rows, acc = {}, 0.0
     for i in dec:
-        if acc + wl.n(i) * row_flops(i) > target and rows:
+        if acc + wl.n(i) * row_flops(i) > target_flops and rows:
             break
         rows[i] = np.arange(wl.n(i))
         acc += wl.n(i) * row_flops(i)
-    left = max(target - acc, 0.0)
+    left = max(target_flops - acc, 0.0)
     if pre:
         per_item = left / len(pre)
         for i in pre:
             k = int(min(wl.n(i), max(1, per_item // row_flops(i))))
             rows[i] = np.linspace(0, wl.n(i) - 1, k).astype(np.int64)
             acc += k * row_flops(i)
+    return rows, acc
+
+
+def cpu_baseline(wl, budget_s, single_thread=True):
+    """The oracle (as it stands) on the host cores, on a bounded sample of the
+    same workload: every block decode, then evenly spaced rows of each prefill,
+    sized so that one run takes about budget_s / 3. A calibration run serves as
+    the warm-up; then three timed runs, whose median gives the rate. Input
+    drawing is not timed. Also one thread on the single-request workload
+    (whole call) and on a sample of the LLaDA decode batch."""
+    import numpy as np
+
+    import workloads
+    from oracle import oracle
+    all_threads = len(os.sched_getaffinity(0))
+    threads = oracle.threads(all_threads)
+    D, Hq = wl.head_dim, wl.num_q_heads
+
+    def timed(call, sel):
+        t0 = time.perf_counter()
+        oracle.run(call, sel)
+        return time.perf_counter() - t0
+
+    def rate_of(w, budget, row_flops):
+        # calibrate on a piece large enough to keep the threads busy
+        dec = [i for i in range(w.num_items) if w.n(i) <= 32]
+        cal_items = dec[:4] if dec else [i for i in range(w.num_items)][:1]
+        cal_rows = {i: np.arange(w.n(i) if w.n(i) <= 32 else min(w.n(i), 64)) for i in cal_items}
+        call = oracle.Call(w, sorted(cal_rows))
+        sel, _, _ = oracle.selection(call, cal_rows)
+        cal = sum(len(r) * row_flops(i) for i, r in cal_rows.items()) / max(timed(call, sel), 1e-6)
+        return cal * budget
+
+    row_flops = lambda i: 4.0 * int(wl.kv_len[i]) * D * Hq
+    rows, acc = _oracle_sample(wl, rate_of(wl, budget_s / 3, row_flops), row_flops)
     call = oracle.Call(wl, sorted(rows))
     sel, _, _ = oracle.selection(call, rows)
-    t = time.perf_counter()
-    oracle.run(call, sel)
-    dt = time.perf_counter() - t
+    times = [timed(call, sel) for _ in range(3)]
+    dt = float(np.median(times))
     n_dec = sum(1 for i in rows if wl.n(i) <= 32)
     n_pre_rows = sum(len(rows[i]) for i in rows if wl.n(i) > 32)
-    cpu = "unknown CPU"
-    try:
-        with open("/proc/cpuinfo") as fh:
-            for line in fh:
-                if line.startswith("model name"):
-                    cpu = line.split(":", 1)[1].strip()
-                    break
-    except OSError:
-        pass
-    total_pre_rows = sum(wl.n(i) for i in pre)
-    sample = (f"{n_dec} of {len(dec)} block decodes (all rows, all heads) and {n_pre_rows} of "
+    total_dec = sum(1 for i in range(wl.num_items) if wl.n(i) <= 32)
+    total_pre_rows = sum(wl.n(i) for i in range(wl.num_items) if wl.n(i) > 32)
+    model = cpu_model()
+    sample = (f"{n_dec} of {total_dec} block decodes (all rows, all heads) and {n_pre_rows} of "
               f"{total_pre_rows} prefill rows, evenly spaced (all heads), of {wl.name} seed {wl.seed}: "
-              f"{acc / 1e9:.1f} GFLOP in {dt:.1f} s, fp64, {threads} threads on {cpu}, "
+              f"{acc / 1e9:.1f} GFLOP, median of 3 runs after a warm-up "
+              f"({', '.join(f'{x:.2f}' for x in times)} s), fp64, {threads} threads on {model}, "
               f"input drawing excluded")
+
+    # one thread: the single-request workload whole, and LLaDA block decodes
+    one = []
+    oracle.threads(1)
+    try:
+        for w, budget in ((workloads.tiny_mixed(0), None), (workloads.llada_decode(0), 3.0)) if single_thread else ():
+            rf = lambda i, w=w: 4.0 * int(w.kv_len[i]) * w.head_dim * w.num_q_heads
+            if budget is None:
+                r1 = {i: np.arange(w.n(i)) for i in range(w.num_items)}
+                a1 = sum(w.n(i) * rf(i) for i in range(w.num_items))
+            else:
+                r1, a1 = _oracle_sample(w, rate_of(w, budget, rf), rf)
+            c1 = oracle.Call(w, sorted(r1))
+            s1, _, _ = oracle.selection(c1, r1)
+            timed(c1, s1)
+            t1 = float(np.median([timed(c1, s1) for _ in range(3)]))
+            one.append({"workload": w.name, "value": a1 / t1 / 1e12, "unit": "TFLOP/s", "cores": 1,
+                        "sample": f"{len(r1)} of {w.num_items} items ({a1 / 1e9:.2f} GFLOP), median of 3 "
+                                  f"after a warm-up: {t1:.3f} s"})
+    finally:
+        oracle.threads(all_threads)
     return {"value": acc / dt / 1e12, "unit": "TFLOP/s", "cores": threads, "kind": "oracle",
-            "sample": sample, "seconds": dt}
+            "sample": sample, "seconds": dt, "cpu": model, "single_thread": one or None}
 
 
 def kernel_source_hash():
@@ -205,7 +264,7 @@ def decode_sweep(args):
                 "decode_launch": "prefill-shaped (heads across)" if fused else "decode-shaped",
                 "splits": int(p.info.num_split_items),
                 "tiles": int(p.info.num_prefill_tiles if fused else p.info.num_decode_tiles),
-                "cpu_baseline": None if args.no_cpu_baseline else cpu_baseline(wl, args.sweep_cpu_budget)}),
+                "cpu_baseline": None if args.no_cpu_baseline else cpu_baseline(wl, args.sweep_cpu_budget, False)}),
                   flush=True)
             del t, out, lse, ws
 
@@ -362,8 +421,8 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="dream_mixed",
-                    choices=["tiny_mixed", "llada_decode", "dream_mixed", "dream_decode", "prefill_heavy",
-                             "long_decode", "token_cache"])
+                    choices=["tiny_mixed", "llada_decode", "dream_mixed", "dream_decode", "dream_prefill",
+                             "prefill_heavy", "long_decode", "token_cache"])
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle work")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -387,11 +446,16 @@ def main():
     ap.add_argument("--trace-rate", type=float, default=0.3, help="requests per iteration (--serve-trace)")
     ap.add_argument("--kv-transfer", action="store_true",
                     help="time the paged-KV export / import of three batches' cached contexts")
-    ap.add_argument("--flush", action="store_true",
-                    help="read 1 GiB of other data between steps (outside the timing) so no step "
-                         "reads the previous one's data from the 256 MB Infinity Cache; steps are "
-                         "then timed by events. A read, not a write: written lines would be "
-                         "written back to HBM during the next step")
+    ap.add_argument("--flushed-reps", type=int, default=50,
+                    help="steps timed after the timed region, each after a 1 GiB read (outside the "
+                         "timing) that evicts the previous step's data from the 256 MB Infinity "
+                         "Cache; reported as median and min. A read, not a write: written lines "
+                         "would be written back to HBM during the next step")
+    ap.add_argument("--no-ceilings", action="store_true",
+                    help="skip the measured HBM-read and MFMA ceilings")
+    ap.add_argument("--ceiling-reps", type=int, default=5)
+    ap.add_argument("--ceilings", action="store_true",
+                    help="instead of a workload: print the measured ceilings as one JSON line")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -407,6 +471,64 @@ def main():
     if args.kv_transfer:
         kv_transfer(args)
         return
+    if args.ceilings:
+        print(json.dumps({"ceilings": measure_ceilings(args)}), flush=True)
+        return
+
+    bench_workload(args)
+
+
+def measure_ceilings(args):
+    """Measured ceilings of the chip (HIP events around one probe launch,
+    median of the reps): a streaming read of a 4 GiB buffer (16 times the
+    256 MB Infinity Cache, so the figure is HBM) and a matrix-core loop of
+    independent bf16 MFMAs."""
+    import numpy as np
+    import torch
+
+    from paper_2607_04206_amd._lib import check, lib
+
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream(dev)
+    res = {}
+    nbytes = 4 << 30
+    buf = torch.ones((nbytes // 4,), dtype=torch.int32, device=dev)
+    grid = 8192
+    sink = torch.empty((grid,), dtype=torch.int32, device=dev)
+    times = []
+    for r in range(3 + args.ceiling_reps):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        check(lib.sangam_probe_hbm_read(buf.data_ptr(), nbytes, sink.data_ptr(), grid, stream.cuda_stream))
+        b.record(stream)
+        b.synchronize()
+        if r >= 3:
+            times.append(a.elapsed_time(b) / 1e3)
+    res["hbm_read_gbs"] = nbytes / float(np.median(times)) / 1e9
+    res["hbm_read"] = "4 GiB streaming read, 16-byte loads, 8192 work-groups of 256 threads"
+    del buf, sink
+    grid, iters = 2048, 2048
+    sinkf = torch.empty((grid,), dtype=torch.float32, device=dev)
+    flops = grid * 4 * iters * 8 * 32768.0
+    times = []
+    for r in range(2 + args.ceiling_reps):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        check(lib.sangam_probe_mfma_bf16(sinkf.data_ptr(), grid, iters, stream.cuda_stream))
+        b.record(stream)
+        b.synchronize()
+        if r >= 2:
+            times.append(a.elapsed_time(b) / 1e3)
+    res["mfma_bf16_tflops"] = flops / float(np.median(times)) / 1e12
+    res["mfma"] = "v_mfma_f32_32x32x16_bf16, 8 independent chains per wave, 2048 work-groups of 4 waves"
+    return res
+
+
+def bench_workload(args):
+    """One workload: warm-up, a per-launch breakdown, the timed region of K
+    back-to-back steps, then R flushed steps (each after a 1 GiB read) timed
+    with events, the measured ceilings and the oracle on a CPU sample."""
+    import ctypes
 
     import numpy as np
     import torch
@@ -420,21 +542,26 @@ def main():
     print(f"[bench] {wl.name} seed {wl.seed}: drawing inputs", file=sys.stderr, flush=True)
     t = workloads.device_inputs(wl, dev, fill=None)
 
-    t0 = time.perf_counter()
-    p = attn.plan(q_indptr=wl.q_indptr, q_offset=wl.q_offset, kv_len=wl.kv_len,
-                  page_indptr=wl.page_indptr, page_ids=wl.page_ids, num_q_heads=wl.num_q_heads,
-                  num_kv_heads=wl.num_kv_heads, head_dim=wl.head_dim,
-                  num_pool_pages=wl.num_pool_pages, sm_scale=wl.sm_scale, q_pos=wl.q_pos)
-    plan_ms = (time.perf_counter() - t0) * 1e3
+    plan_kw = dict(q_indptr=wl.q_indptr, q_offset=wl.q_offset, kv_len=wl.kv_len, page_indptr=wl.page_indptr,
+                   page_ids=wl.page_ids, num_q_heads=wl.num_q_heads, num_kv_heads=wl.num_kv_heads,
+                   head_dim=wl.head_dim, num_pool_pages=wl.num_pool_pages, sm_scale=wl.sm_scale, q_pos=wl.q_pos)
+    attn.plan(**plan_kw)  # first call sizes the binding's planning buffer
+    plan_times = []
+    for _ in range(5):
+        t0 = time.perf_counter()
+        p = attn.plan(**plan_kw)
+        plan_times.append((time.perf_counter() - t0) * 1e3)
+    plan_ms = float(np.median(plan_times))
     p.to(dev)
     T, Hq, D = wl.total_q, wl.num_q_heads, wl.head_dim
     out = torch.empty((T, Hq, D), dtype=torch.bfloat16, device=dev)
     lse = torch.empty((T, Hq), dtype=torch.float32, device=dev)
     ws = torch.empty((max(p.workspace_bytes, 16),), dtype=torch.uint8, device=dev)
     stream = torch.cuda.current_stream(dev)
-    import ctypes
     args_c = attn.c_args(p, t["q"], t["k_new"], t["v_new"], t["k_cache"], t["v_cache"], t["page_ids"],
                          out, lse, ws, stream)
+    ran = {"prefill_attn": p.info.num_prefill_tiles > 0, "decode_attn": p.info.num_decode_tiles > 0,
+           "merge": p.info.num_split_items > 0}
 
     def make_events(which=range(3)):
         """Start / stop event pairs of the three launches; launches outside
@@ -446,7 +573,7 @@ def main():
         arr = (ctypes.c_void_p * 6)(*[e.cuda_event if e is not None else None for e in evs])
         return evs, arr
 
-    flush_buf = torch.ones((1 << 28,), dtype=torch.float32, device=dev) if args.flush else None
+    flush_buf = torch.ones((1 << 28,), dtype=torch.float32, device=dev)  # 1 GiB, read between flushed steps
     if args.copy_calib_mib > 0:
         src = torch.ones((args.copy_calib_mib << 20,), dtype=torch.uint8, device=dev)
         dst = torch.empty_like(src)
@@ -460,64 +587,94 @@ def main():
     torch.cuda.synchronize()
     print(f"[bench] warmup done ({args.warmup} steps)", file=sys.stderr, flush=True)
 
-    # phase breakdown, outside the timed region: events on all three launches
+    # per-launch breakdown, outside the timed region: events on all three
+    # launches; a launch with no work reports null
     K = args.steps
     n_phase = max(3, min(K, 10))
     evsets = [make_events() for _ in range(n_phase)]
     torch.cuda.synchronize()
     for k in range(n_phase):
-        if args.flush:
-            flush_buf.sum()
         check(lib.sangam_attn_forward_timed(*args_c, evsets[k][1]))
     torch.cuda.synchronize()
     phase_ms = {}
     for j, name in enumerate(PHASES):
-        phase_ms[name] = float(np.mean([evsets[k][0][2 * j].elapsed_time(evsets[k][0][2 * j + 1])
-                                        for k in range(n_phase)]))
+        phase_ms[name] = (float(np.mean([evsets[k][0][2 * j].elapsed_time(evsets[k][0][2 * j + 1])
+                                         for k in range(n_phase)])) if ran[name] else None)
     work = split_work(wl, fused_decodes=int(p.info.num_fused_decode_tiles) > 0)
-    dom = max(("prefill_attn", "decode_attn"), key=lambda n: phase_ms[n] if work[n][0] > 0 else -1)
+    dom = max((n for n in ("prefill_attn", "decode_attn") if ran[n]), key=lambda n: phase_ms[n])
     jd = PHASES.index(dom)
 
-    # timed region: K whole steps; only the dominant launch carries events
+    # timed region: K whole steps back to back; only the dominant launch
+    # carries events (in its dispatch)
     evsets = [make_events((jd,)) for _ in range(K)]
     torch.cuda.synchronize()
-    if args.flush:
-        step_ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-                   for _ in range(K)]
-        for k in range(K):
-            flush_buf.sum()
-            step_ev[k][0].record(stream)
-            check(lib.sangam_attn_forward_timed(*args_c, evsets[k][1]))
-            step_ev[k][1].record(stream)
-        torch.cuda.synchronize()
-        ms_per_step = float(np.mean([a.elapsed_time(b) for a, b in step_ev]))
-    else:
-        torch.cuda.synchronize()
-        w0 = time.perf_counter()
-        for k in range(K):
-            check(lib.sangam_attn_forward_timed(*args_c, evsets[k][1]))
-        torch.cuda.synchronize()
-        ms_per_step = (time.perf_counter() - w0) * 1e3 / K
-    dom_ms = float(np.mean([evsets[k][0][2 * jd].elapsed_time(evsets[k][0][2 * jd + 1]) for k in range(K)]))
+    w0 = time.perf_counter()
+    for k in range(K):
+        check(lib.sangam_attn_forward_timed(*args_c, evsets[k][1]))
+    torch.cuda.synchronize()
+    ms_per_step = (time.perf_counter() - w0) * 1e3 / K
+    dom_all = np.array([evsets[k][0][2 * jd].elapsed_time(evsets[k][0][2 * jd + 1]) for k in range(K)])
     print(f"[bench] timed {K} steps: {ms_per_step:.4f} ms/step", file=sys.stderr, flush=True)
+
+    # flushed protocol: before each rep a 1 GiB read (outside the timing)
+    # evicts the previous rep's data from the 256 MB Infinity Cache; the step
+    # and the dominant launch are timed with events
+    R = max(args.flushed_reps, 0)
+    evsets = [make_events((jd,)) for _ in range(R)]
+    step_ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(R)]
+    torch.cuda.synchronize()
+    for k in range(R):
+        flush_buf.sum()
+        step_ev[k][0].record(stream)
+        check(lib.sangam_attn_forward_timed(*args_c, evsets[k][1]))
+        step_ev[k][1].record(stream)
+    torch.cuda.synchronize()
+    fl_step = np.array([a.elapsed_time(b) for a, b in step_ev])
+    fl_dom = np.array([evsets[k][0][2 * jd].elapsed_time(evsets[k][0][2 * jd + 1]) for k in range(R)])
+    if R:
+        print(f"[bench] flushed {R} steps: median {np.median(fl_step):.4f} ms", file=sys.stderr, flush=True)
+    del flush_buf
 
     F, B = wl.flops(), wl.hbm_bytes()
     sec = ms_per_step / 1e3
     tflops, gbs = F / sec / 1e12, B / sec / 1e9
     t_star = max(F / (PEAK_BF16_TFLOPS * 1e12), B / (PEAK_HBM_GBS * 1e9))
 
+    ceil = None
+    if not args.no_ceilings:
+        print("[bench] measuring the chip's ceilings", file=sys.stderr, flush=True)
+        ceil = measure_ceilings(args)
+
     f_d, b_d = work[dom]
+    dom_ms = float(dom_all.mean())
     t_d = dom_ms / 1e3
     intensity = f_d / max(b_d, 1.0)
     if intensity >= PEAK_BF16_TFLOPS * 1e12 / (PEAK_HBM_GBS * 1e9):
-        roof = {"bound": "mfma", "achieved": f_d / t_d / 1e12, "peak": PEAK_BF16_TFLOPS,
-                "unit": "TFLOP/s"}
+        roof = {"bound": "mfma", "achieved": f_d / t_d / 1e12, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s"}
+        rate = lambda ms: f_d / (ms / 1e3) / 1e12
+        measured_peak = ceil["mfma_bf16_tflops"] if ceil else None
     else:
         roof = {"bound": "hbm", "achieved": b_d / t_d / 1e9, "peak": PEAK_HBM_GBS, "unit": "GB/s"}
+        rate = lambda ms: b_d / (ms / 1e3) / 1e9
+        measured_peak = ceil["hbm_read_gbs"] if ceil else None
     roof["frac"] = roof["achieved"] / roof["peak"]
     roof["traffic"] = measured_traffic(wl.name, dom)
     roof["kernel"] = dom
     roof["kernel_ms"] = dom_ms
+    roof["kernel_ms_median"] = float(np.median(dom_all))
+    roof["kernel_ms_min"] = float(dom_all.min())
+    roof["flushed"] = None
+    if R:
+        roof["flushed"] = {"kernel_ms_median": float(np.median(fl_dom)), "kernel_ms_min": float(fl_dom.min()),
+                           "achieved_median": rate(float(np.median(fl_dom))),
+                           "frac_median": rate(float(np.median(fl_dom))) / roof["peak"],
+                           "step_ms_median": float(np.median(fl_step)), "step_ms_min": float(fl_step.min()),
+                           "reps": R, "flush": "1 GiB read between reps, outside the timing"}
+    if measured_peak:
+        roof["measured_peak"] = measured_peak
+        roof["frac_of_measured"] = roof["achieved"] / measured_peak
+        if R:
+            roof["flushed"]["frac_of_measured_median"] = roof["flushed"]["achieved_median"] / measured_peak
     roof["algorithmic_flops"] = f_d
     roof["algorithmic_bytes"] = b_d
 
@@ -544,7 +701,7 @@ def main():
                    "prefills": wl.num_items - n_dec, "num_q_heads": wl.num_q_heads,
                    "num_kv_heads": wl.num_kv_heads, "head_dim": wl.head_dim, "page_size": 16,
                    "query_rows": T, "context_tokens": int(wl.kv_len.sum()),
-                   "parallelism": "1 GPU", "mall_flush": bool(args.flush)},
+                   "parallelism": "1 GPU"},
         "tflops": tflops,
         "hbm_gbs": gbs,
         "mfma_frac": tflops / PEAK_BF16_TFLOPS,
@@ -552,14 +709,16 @@ def main():
         "roofline_frac": t_star / sec,
         "algorithmic_flops": F,
         "algorithmic_bytes": B,
+        "flushed_step_ms_median": float(np.median(fl_step)) if R else None,
+        "flushed_step_ms_min": float(fl_step.min()) if R else None,
         "phase_ms": phase_ms,
         "plan_ms": plan_ms,
         "kernel_source_hash": kernel_source_hash(),
+        "ceilings": ceil,
         "roofline": roof,
         "cpu_baseline": cpu,
     }
     print(json.dumps(res), flush=True)
-
 
 if __name__ == "__main__":
     main()

@@ -1,5 +1,5 @@
-"""ctypes declarations of the C ABI in include/sangam_attn.h, sangam_sched.h
-and sangam_kv.h.
+"""ctypes declarations of the C ABI in include/sangam_attn.h, sangam_sched.h,
+sangam_kv.h and sangam_probe.h.
 
 Loads the in-tree ``libsangam_attn.so``; there is no fallback: if the
 library is missing or does not load, importing this module raises.
@@ -45,6 +45,8 @@ EXPORTS = (
     "sangam_kv_plan_rows",
     "sangam_kv_export",
     "sangam_kv_import",
+    "sangam_probe_hbm_read",
+    "sangam_probe_mfma_bf16",
 )
 
 
@@ -140,6 +142,10 @@ def _load():
     lib.sangam_kv_export.restype = ctypes.c_int32
     lib.sangam_kv_import.argtypes = [P, P, P, P, P, P, P]
     lib.sangam_kv_import.restype = ctypes.c_int32
+    lib.sangam_probe_hbm_read.argtypes = [P, S, P, ctypes.c_int32, P]
+    lib.sangam_probe_hbm_read.restype = ctypes.c_int32
+    lib.sangam_probe_mfma_bf16.argtypes = [P, ctypes.c_int32, ctypes.c_int32, P]
+    lib.sangam_probe_mfma_bf16.restype = ctypes.c_int32
     lib.sangam_last_error.argtypes = []
     lib.sangam_last_error.restype = ctypes.c_char_p
     lib.sangam_version.argtypes = []

@@ -9,7 +9,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libsangam_attn.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
-SOURCES = ["plan.cpp", "sched.cpp", "kv_plan.cpp", "attn_fwd.hip", "kv_copy.hip"]
+SOURCES = ["plan.cpp", "sched.cpp", "kv_plan.cpp", "attn_fwd.hip", "kv_copy.hip", "probe.hip"]
 
 FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",

@@ -22,9 +22,20 @@ def test_more_than_one_gpu_is_refused():
 
 def test_decode_point_oracle_leg():
     wl = workloads.decode_sweep("llada", 1, 0)
-    r = bench.cpu_baseline(wl, 0.2)
+    r = bench.cpu_baseline(wl, 0.2, single_thread=False)
     assert r["kind"] == "oracle" and r["unit"] == "TFLOP/s" and r["value"] > 0 and r["cores"] >= 1
-    assert "1 of 1 block decodes" in r["sample"]
+    assert "1 of 1 block decodes" in r["sample"] and "median of 3" in r["sample"]
+    assert r["single_thread"] is None
+    json.dumps(r)
+
+
+def test_oracle_leg_single_thread_runs():
+    wl = workloads.tiny_mixed(0)
+    r = bench.cpu_baseline(wl, 0.3)
+    names = [x["workload"] for x in r["single_thread"]]
+    assert names == ["tiny_mixed", "llada_decode"]
+    assert all(x["cores"] == 1 and x["value"] > 0 for x in r["single_thread"])
+    assert r["cpu"] and r["cores"] == len(os.sched_getaffinity(0))
     json.dumps(r)
 
 

@@ -449,6 +449,16 @@ def dream_decode(seed: int = 0) -> Workload:
     return make_workload("dream_decode", seed, hq=28, hkv=4, d=128, decodes=dec, prefills=[], rng=rng)
 
 
+def dream_prefill(seed: int = 0) -> Workload:
+    """The two whole prefills of dream_mixed (L = 2304 and 3328; GQA 28/4,
+    D 128) alone: the batch's compute-bound part, profiled apart from its
+    block decodes."""
+    rng = np.random.default_rng(seed)
+    _lognormal_lengths(rng, 48, 500, 0.8, 16, 4096)  # the same draws as dream_mixed, so the same pages
+    rng.integers(0, 256 // BLOCK, size=48)
+    return make_workload("dream_prefill", seed, hq=28, hkv=4, d=128, decodes=[], prefills=[2304, 3328], rng=rng)
+
+
 def prefill_heavy(seed: int = 0) -> Workload:
     """Long-document prefills: GQA 28/4, D 128; 8 whole prefills with prompts
     ~ LN(6000, 0.5) in [1024, 16384] + 256 response; KV written to pages."""
@@ -477,6 +487,7 @@ WORKLOADS = {
     "llada_decode": llada_decode,
     "dream_mixed": dream_mixed,
     "dream_decode": dream_decode,
+    "dream_prefill": dream_prefill,
     "prefill_heavy": prefill_heavy,
     "long_decode": long_decode,
 }
