@@ -172,7 +172,9 @@ __global__ __launch_bounds__(64 * QW * KW, MINB) void attn_tiles_kernel(AttnArgs
     static_assert(KW == 1 || (QW * (KW - 1) * MERGE_REGS * 64 * 4) <= 2 * NSTAGE * TILE,
                   "cross-wave merge must fit in the stage buffers");
     static_assert(NSTAGE >= 2 && NSTAGE <= 4, "2 to 4 stage buffers");
-    static_assert(HEADS_ACROSS || 32 * QB * QW <= 240, "a tile writes back at most 16 pages");
+    // pages a tile's write-back range can touch: its rows at any offset
+    constexpr int WPAGES = HEADS_ACROSS ? 16 : (32 * QB * QW + 15) / 16 + 1;
+    static_assert(WPAGES <= NT, "one thread per write-back page id");
     // with more than two buffers the wait counts loads, so every wave must
     // issue the same number per stage
     static_assert(NSTAGE == 2 || NCH % NT == 0, "deeper pipelines need whole staging rounds");
@@ -182,7 +184,7 @@ __global__ __launch_bounds__(64 * QW * KW, MINB) void attn_tiles_kernel(AttnArgs
     __shared__ int32_t pages[MAX_PAGES];
     __shared__ uint32_t pinfo[MAX_PAGES];  // page_info of the tile's pages (kItemPosList items)
     __shared__ int32_t fpos[kWaveRows];    // the listed positions (kItemPosList items)
-    __shared__ int32_t wpages[16];  // pages of the fresh rows this tile writes back
+    __shared__ int32_t wpages[WPAGES];  // pages of the fresh rows this tile writes back
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -915,10 +917,17 @@ static sangam_status forward_impl(const void* plan_host, const void* plan_dev, c
     // decode-shaped tiles; both also write the fresh rows into their pages
     if (h->n_prefill_tiles > 0) {
         args.tiles = reinterpret_cast<const TileRec*>(pd + h->off_prefill_tiles);
-        hipError_t e =
-            h->d == 128
-                ? launch_tiles<128, kPrefillQWaves, 1, kPrefillQBlocks, 2, false>(args, h->n_prefill_tiles, stream, evs(0))
-                : launch_tiles<64, kPrefillQWaves, 1, kPrefillQBlocks, 2, false>(args, h->n_prefill_tiles, stream, evs(0));
+        hipError_t e;
+        if (h->prefill_rows == kWidePrefillRows && h->d == 128)
+            e = launch_tiles<128, kWidePrefillQWaves, 1, 1, 4, false>(args, h->n_prefill_tiles, stream, evs(0));
+        else if (h->prefill_rows == kPrefillRows)
+            e = h->d == 128
+                    ? launch_tiles<128, kPrefillQWaves, 1, kPrefillQBlocks, 2, false>(args, h->n_prefill_tiles, stream, evs(0))
+                    : launch_tiles<64, kPrefillQWaves, 1, kPrefillQBlocks, 2, false>(args, h->n_prefill_tiles, stream, evs(0));
+        else {
+            set_error("no prefill kernel for this tile shape");
+            return SANGAM_ERR_UNSUPPORTED;
+        }
         if (e != hipSuccess) return hip_fail(e, "prefill attention launch");
     } else if (hipError_t e = mark_empty(0); e != hipSuccess) {
         return hip_fail(e, "event record");

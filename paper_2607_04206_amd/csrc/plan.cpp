@@ -13,7 +13,10 @@
 //                  group, extra waves split the chunk further.
 //   prefill-shaped (n_i > 32, a whole prefill): one work-group per (item,
 //                  query head, 128-row block); four waves of 32 rows share
-//                  each staged K/V tile.
+//                  each staged K/V tile. At head_dim 128, when no block
+//                  decode joins this launch and every such item is long, the
+//                  wide shape instead: 256-row blocks on eight waves with
+//                  128-key stages (one work-group per CU).
 // In a batch that holds prefills, block decodes whose GQA group has at least
 // four query heads are cut into prefill-shaped work-groups instead (one query
 // head per wave, kTileHeadsAcross): they join the prefill launch, where the
@@ -224,6 +227,16 @@ extern "C" sangam_status sangam_attn_plan(const sangam_attn_desc* d, void* plan_
                                                    kKeyAlign)));
     }
     if (fuse) decode_keys = decode_units = 0;  // no decode-shaped work-group
+    // prefill-shaped tiles: the wide (eight-wave, 128-key stage) shape when
+    // the launch holds no fused block decodes (they take one query head per
+    // wave of a four-wave tile) and every prefill-shaped item is long, so
+    // that few of the 256-row tiles run part-empty
+    bool wide = D == 128 && has_prefill;
+    for (int i = 0; i < n_items && wide; ++i) {
+        const int64_t n = int64_t(d->q_indptr[i + 1]) - d->q_indptr[i];
+        if (n > kWaveRows ? n < kWidePrefillMinRows : fuse) wide = false;
+    }
+    const int prefill_rows = wide ? kWidePrefillRows : kPrefillRows;
     // While the unsplit decode work-groups would leave CUs idle (a small
     // batch: fewer than two MHA work-groups, or one GQA work-group, per CU),
     // a call is bound by the latency of each work-group's stage chain, not by
@@ -333,7 +346,7 @@ extern "C" sangam_status sangam_attn_plan(const sangam_attn_desc* d, void* plan_
             const ItemRec& it = items[i];
             if (it.n <= kWaveRows && fuse) np += int64_t(it.num_splits) * hkv * fused_tiles_per_kv_head;
             else if (it.n <= kWaveRows) nd += int64_t(it.num_splits) * hkv * tiles_per_kv_head;
-            else np += int64_t(it.num_splits) * hq * ceil_div(it.n, kPrefillRows);
+            else np += int64_t(it.num_splits) * hq * ceil_div(it.n, prefill_rows);
         }
         dec.reserve(size_t(nd)); dec_cost.reserve(size_t(nd));
         pre.reserve(size_t(np)); pre_cost.reserve(size_t(np));
@@ -360,12 +373,12 @@ extern "C" sangam_status sangam_attn_plan(const sangam_attn_desc* d, void* plan_
                         dec_cost.push_back(int64_t(ke - kb));
                     }
             } else {
-                const int nrb = int(ceil_div(it.n, kPrefillRows));
+                const int nrb = int(ceil_div(it.n, prefill_rows));
                 for (int h = 0; h < hq; ++h)
                     for (int rb = 0; rb < nrb; ++rb) {
-                        TileRec tr{i, h / G, h, rb * kPrefillRows, kb, ke, s, 0};
+                        TileRec tr{i, h / G, h, rb * prefill_rows, kb, ke, s, 0};
                         pre.push_back(tr);
-                        const int rows = std::min(kPrefillRows, it.n - rb * kPrefillRows);
+                        const int rows = std::min(prefill_rows, it.n - rb * prefill_rows);
                         pre_cost.push_back(int64_t(ke - kb) * ((rows + kWaveRows - 1) / kWaveRows));
                     }
             }
@@ -434,11 +447,11 @@ extern "C" sangam_status sangam_attn_plan(const sangam_attn_desc* d, void* plan_
     h.decode_kw = kw;
     h.decode_nb = qw == 1 ? 1 : 2;
     h.n_prefill_tiles = int32_t(pre.size());
-    h.prefill_nb = 2;
+    h.prefill_nb = wide ? 4 : 2;
     h.n_merge_rows = n_merge;
     h.num_split_items = n_split_items;
     h.max_splits = max_splits;
-    h.prefill_rows = kPrefillRows;
+    h.prefill_rows = prefill_rows;
     h.n_fused_decode_tiles = int32_t(n_fused * hkv * fused_tiles_per_kv_head);
     h.workspace_bytes = ws_floats * int64_t(sizeof(float));
     h.off_items = off_items;

@@ -15,6 +15,13 @@ constexpr int kWaveRows = 32;       // query rows held by one wave (one decode b
 constexpr int kPrefillQWaves = 4;   // waves of a prefill-shaped work-group
 constexpr int kPrefillQBlocks = 1;  // 32-row query blocks per prefill wave
 constexpr int kPrefillRows = kWaveRows * kPrefillQBlocks * kPrefillQWaves;
+// Wide prefill-shaped work-groups (head_dim 128, batches whose prefill
+// launch holds no fused block decodes and only long prefill-shaped items):
+// eight waves of 32 rows of one query head, 128-key stages, one work-group
+// per CU; half the barriers per key of the four-wave tile.
+constexpr int kWidePrefillQWaves = 8;
+constexpr int kWidePrefillRows = kWaveRows * kWidePrefillQWaves;
+constexpr int kWidePrefillMinRows = 1024;  // every prefill-shaped item at least this long
 constexpr int kKeyAlign = 64;       // split boundaries are multiples of this many keys
 constexpr int kForcedSplitLen = 8192;  // a decode context longer than this is always split
 // Longest context range of one tile that reads cached (paged) rows: the
@@ -104,7 +111,7 @@ struct PlanHeader {
     int32_t n_merge_rows;
     int32_t num_split_items;
     int32_t max_splits;
-    int32_t prefill_rows;  // query rows per prefill-shaped tile
+    int32_t prefill_rows;  // query rows per prefill-shaped tile: kPrefillRows or kWidePrefillRows
     int32_t n_fused_decode_tiles;
     int32_t reserved;
     int64_t workspace_bytes;

@@ -287,6 +287,25 @@ def test_cached_multi_row_blocks(dev, hq, hkv, d, with_decodes, force):
     check_pool_untouched(wl, t)
 
 
+@pytest.mark.parametrize("hq,hkv", [(28, 4), (32, 32), (8, 8)])
+@pytest.mark.parametrize("force", [0, 2])
+def test_wide_prefill_tiles(dev, hq, hkv, force):
+    """The wide prefill-shaped tile (256 rows on eight waves, 128-key stages),
+    which a batch of only long prefill-shaped items takes at head_dim 128:
+    ragged row and key tails, a long cached block at an unaligned offset over
+    a context past the cached-range limit, with and without forced splits;
+    every row against the oracle, the cache bit for bit."""
+    wl = workloads.make_workload("wide", 41, hq=hq, hkv=hkv, d=128, prefills=[1024, 1500, 2049],
+                                 decodes=[(37, 9000, 1100), (0, 1300, 1029)])
+    p, t, out, lse = run(wl, dev, force_splits=force)
+    assert p.info.num_decode_tiles == 0 and p.info.num_fused_decode_tiles == 0
+    from tests.test_plan import parse
+    assert int(parse(p)[0]["prefill_rows"]) == 256
+    check_full(wl, out, lse)
+    check_cache(wl, t)
+    check_pool_untouched(wl, t)
+
+
 def test_sequential_prefill_then_decode(dev):
     """The cached-dLLM cycle in two calls (the single-request workload's
     sequential reading): a prefill call writes the request's pages, then a

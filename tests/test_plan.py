@@ -453,3 +453,20 @@ def test_cached_multi_row_blocks_plan(hq, hkv):
     # item 0: 1 row block, items 1 and 2: 2 row blocks of 128, each split in two
     assert list(per_item) == [hq, 2 * 2 * hq, 2 * 2 * hq]
     assert len(mer) == 200 + 150
+
+
+def test_wide_prefill_tiles_chosen():
+    """256-row prefill-shaped tiles exactly when head_dim is 128, no block
+    decode joins the prefill launch and every prefill-shaped item has at
+    least 1024 rows."""
+    def rows(wl):
+        return int(parse(plan_of(wl))[0]["prefill_rows"])
+    mk = lambda **kw: workloads.make_workload("w", 2, **kw)
+    assert rows(workloads.prefill_heavy(0)) == 256
+    assert rows(workloads.dream_prefill(0)) == 256
+    assert rows(workloads.dream_mixed(0)) == 128           # fused block decodes
+    assert rows(mk(hq=8, hkv=8, d=128, decodes=[(5, 900)], prefills=[2000])) == 256  # MHA decodes stay apart
+    assert rows(mk(hq=28, hkv=4, d=128, decodes=[(5, 900)], prefills=[2000])) == 128  # GQA decodes fuse
+    assert rows(mk(hq=8, hkv=8, d=128, decodes=[], prefills=[2000, 1023])) == 128     # a short prefill
+    assert rows(mk(hq=8, hkv=8, d=64, decodes=[], prefills=[2000])) == 128            # head_dim 64
+    assert rows(mk(hq=8, hkv=8, d=128, decodes=[(37, 9000, 1100)], prefills=[])) == 256  # long cached block
