@@ -198,8 +198,8 @@ __global__ __launch_bounds__(64 * QW * KW, MINB) void attn_tiles_kernel(AttnArgs
     const ItemRec it = a.items[t.item];
     // heads across the waves: a decode-shaped work-group, or a block decode
     // cut into a prefill-shaped one (whose last tile of a GQA group may hold
-    // fewer heads than waves: the extra waves compute with the tile's first
-    // head and store nothing)
+    // fewer heads than waves: the extra waves only stage K/V, write back and
+    // meet the barriers; they compute and store nothing)
     const bool across = HEADS_ACROSS || (t.flags & kTileHeadsAcross);
     const int head_want = across ? t.q_head0 + qs : t.q_head0;
     const bool head_ok = head_want < (t.kv_head + 1) * (a.hq / a.hkv);
@@ -590,17 +590,21 @@ __global__ __launch_bounds__(64 * QW * KW, MINB) void attn_tiles_kernel(AttnArgs
         __syncthreads();
         if (st + NSTAGE - 1 < nstages) issue_stage(st + NSTAGE - 1, (st + NSTAGE - 1) % NSTAGE);
         if (writer) write_back(st);
-        f32x16 sc[QB][NB];
-        qk(st, sc);
-        softmax_pv(st, sc, false);
+        if (head_ok) {  // a wave past its tile's GQA group only stages and writes back
+            f32x16 sc[QB][NB];
+            qk(st, sc);
+            softmax_pv(st, sc, false);
+        }
     }
     if (st < nstages) {  // the last, partial stage
         asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
         __syncthreads();
         if (writer) write_back(st);
-        f32x16 sc[QB][NB];
-        qk(st, sc);
-        softmax_pv(st, sc, true);
+        if (head_ok) {
+            f32x16 sc[QB][NB];
+            qk(st, sc);
+            softmax_pv(st, sc, true);
+        }
     }
 
     // ---- combine the context sub-ranges of the waves that share query rows
