@@ -257,7 +257,7 @@ def decode_sweep(args):
             print(json.dumps({
                 "sweep": "decode_batch", "shape": shape, "num_q_heads": wl.num_q_heads,
                 "num_kv_heads": wl.num_kv_heads, "batch": B, "kv_len": 1024, "ms_per_call": ms,
-                "decode_kernel_ms": kern, "merge_ms": float(launches[2]),
+                "decode_kernel_ms": kern, "merge_ms": float(launches[2]) if p.info.num_split_items > 0 else None,
                 "tflops": F / (ms / 1e3) / 1e12, "hbm_gbs": Bytes / (ms / 1e3) / 1e9,
                 "kernel_hbm_frac": Bytes / (kern / 1e3) / (PEAK_HBM_GBS * 1e9),
                 "kernel_mfma_frac": F / (kern / 1e3) / (PEAK_BF16_TFLOPS * 1e12),
