@@ -1,7 +1,8 @@
 """GPU parity on randomly drawn ragged batches (fixed seeds): head shapes from
 MHA to 11 query heads per KV head, D 64 / 128, block decodes at random block
 offsets (partial blocks and pages included), per-token position lists,
-prefills, forced split counts and small CU counts (which move small
+prefills, cached blocks of more than 32 rows, long prefills that take the
+wide 256-row tile, forced split counts and small CU counts (which move small
 decode-only GQA batches to heads-across tiles and change the split rules).
 Each batch runs through the C ABI and is compared with the fp64 oracle on
 every output element, LSE and written cache row."""
@@ -11,6 +12,7 @@ import torch
 
 import workloads
 from tests.test_parity import check_cache, check_full, check_pool_untouched
+from tests.test_plan import parse
 
 N_CASES = 120
 SHAPES = [(4, 4), (8, 4), (12, 4), (28, 4), (32, 8), (16, 2), (11, 1), (8, 1), (6, 6), (24, 8)]
@@ -32,6 +34,18 @@ def random_batch(seed):
     prefills = [int(rng.integers(1, 400)) for _ in range(int(rng.integers(0 if decodes or pos else 1, 3)))]
     force = int(rng.choice([0, 0, 0, 1, 2, 3, 7]))
     cus = int(rng.choice([0, 8, 64, 256]))
+    # cached blocks of more than 32 rows (larger decode blocks, a block from 0
+    # under a cached tail), or long prefills alone for the wide tile
+    if rng.random() < 0.15:
+        d = 128
+        prefills = [int(rng.integers(1024, 2000)) for _ in range(int(rng.integers(1, 3)))]
+        if hq // hkv >= 4:
+            decodes, pos = [], []
+    else:
+        for _ in range(int(rng.integers(0, 3))):
+            L = int(rng.integers(34, 3000))
+            n = int(rng.integers(33, min(300, L) + 1))
+            decodes.append((int(rng.integers(0, L - n + 1)), L, n))
     wl = workloads.make_workload(f"random_{seed}", seed, hq=hq, hkv=hkv, d=d, decodes=decodes,
                                  prefills=prefills, pos_decodes=pos, rng=rng)
     return wl, force, cus
@@ -85,5 +99,10 @@ def test_random_batches_reach_every_path():
             seen.add("positions")
         if i.num_prefill_tiles > i.num_fused_decode_tiles:
             seen.add("prefill")
-    assert {"split", "positions", "prefill", "fused_with_prefill", "fused_alone"} <= seen, seen
+        if any(wl.n(k) > 32 and not wl.is_prefill[k] for k in range(wl.num_items)):
+            seen.add("cached_block")
+        if int(parse(p)[0]["prefill_rows"]) == 256:
+            seen.add("wide")
+    assert {"split", "positions", "prefill", "fused_with_prefill", "fused_alone", "cached_block",
+            "wide"} <= seen, seen
     assert sum(s.startswith("decode_qw") for s in seen) >= 3, seen

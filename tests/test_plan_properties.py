@@ -1,5 +1,6 @@
 """Randomised planner properties (hypothesis): for arbitrary ragged batches
-(block decodes, per-token position lists, prefills), head shapes, forced
+(block decodes, cached blocks of more than 32 rows, per-token position
+lists, prefills), head shapes, forced
 split counts and CU counts, the plan's work-groups tile every (query head,
 row, key) of every item exactly once, respect the range limit of tiles that
 read cached rows, list exactly the rows of split items for the merge, and
@@ -34,6 +35,10 @@ def batches(draw):
         k = draw(st.integers(1, min(32, L - 1)))
         p = sorted(draw(st.sets(st.integers(0, L - 1), min_size=k, max_size=k)))
         pos.append((p, L))
+    for _ in range(draw(st.integers(0, 2))):  # cached blocks of more than 32 rows
+        L = draw(st.integers(34, 20000))
+        n = draw(st.integers(33, min(300, L)))
+        decodes.append((draw(st.integers(0, L - n)), L, n))
     prefills = [draw(st.integers(1, 700)) for _ in range(n_pre)]
     force = draw(st.sampled_from([0, 0, 0, 1, 2, 3, 7]))
     cus = draw(st.sampled_from([0, 8, 64, 256]))
