@@ -30,6 +30,8 @@ class Plan:
     total_q: int
     num_pool_pages: int = 0  # pool size the plan's page ids were checked against
     total_pages: int = 0     # entries of page_ids the kernels read
+    upload_stream: Optional[torch.cuda.Stream] = None  # the stream the device copy was issued on
+    upload_done: Optional[torch.cuda.Event] = None     # recorded on it after the copy
 
     @property
     def workspace_bytes(self) -> int:
@@ -49,13 +51,30 @@ class Plan:
     def to(self, device) -> "Plan":
         """Copy the blob to device memory (the caller's H2D copy of plan_dev):
         staged through pinned host memory and copied without blocking on the
-        current stream, which later launches on that stream follow. torch's
-        pinned-memory pool keeps the staging buffer until the copy is done."""
+        device's current stream, after which an event is recorded there.
+        Launches on that stream follow the copy; a forward on another stream
+        waits for the event first. torch's pinned-memory pool keeps the
+        staging buffer until the copy is done."""
         dev = torch.device(device)
         pinned = torch.from_numpy(self.host).pin_memory()
         self.dev = torch.empty(pinned.shape, dtype=pinned.dtype, device=dev)
+        self.upload_stream = torch.cuda.current_stream(dev)
         self.dev.copy_(pinned, non_blocking=True)
+        self.upload_done = torch.cuda.Event()
+        self.upload_done.record(self.upload_stream)
         return self
+
+    def order_after_upload(self, stream: torch.cuda.Stream) -> None:
+        """Make `stream` wait for the plan's device copy when the copy was
+        issued on another stream. Under graph capture nothing is waited for
+        (a wait on an event recorded outside the capture is not allowed):
+        the plan must then be resident before the capture starts, e.g. after
+        a synchronisation or an eager call on the capturing stream."""
+        if self.upload_done is None or stream == self.upload_stream:
+            return
+        if torch.cuda.is_current_stream_capturing():
+            return
+        stream.wait_event(self.upload_done)
 
 
 def make_desc(*, q_indptr, q_offset, kv_len, page_indptr, page_ids, num_q_heads, num_kv_heads,
@@ -183,6 +202,7 @@ def forward(p: Plan, q: torch.Tensor, k_new: torch.Tensor, v_new: torch.Tensor,
     if wsb > 0 and workspace is None:
         workspace = torch.empty((wsb,), dtype=torch.uint8, device=dev)
     s = stream if stream is not None else torch.cuda.current_stream(dev)
+    p.order_after_upload(s)
     args = c_args(p, q, k_new, v_new, k_cache, v_cache, page_ids, out, lse, workspace, s)
     if launch_events is None:
         check(lib.sangam_attn_forward(*args))
@@ -218,6 +238,7 @@ def forward_noalloc(p: Plan, q: torch.Tensor, k_new: torch.Tensor, v_new: torch.
     if p.dev is None or p.dev.device != dev:
         raise ValueError("the plan is not on the device: call Plan.to(device) first")
     s = stream if stream is not None else torch.cuda.current_stream(dev)
+    p.order_after_upload(s)
     args = c_args(p, q, k_new, v_new, k_cache, v_cache, page_ids, out, lse, None, s)
     # the same arguments without the workspace pointer and size
     check(lib.sangam_attn_forward_noalloc(*args[:12], args[14]))

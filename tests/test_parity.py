@@ -447,6 +447,27 @@ def test_forward_checks_pool_and_page_table(dev):
         attn.forward(p, t["q"], t["k_new"], t["v_new"], t["k_cache"], t["v_cache"], t["page_ids"][:-1])
 
 
+def test_forward_on_another_stream_follows_the_plan_upload(dev):
+    """The plan is copied to the device without blocking on the current
+    stream; a forward issued right away on another stream waits for that
+    copy (the binding orders it after the upload's event)."""
+    from paper_2607_04206_amd import attn
+    wl = workloads.ragged_small(6, hq=8, hkv=2, d=128)
+    t = workloads.device_inputs(wl, dev)
+    torch.cuda.synchronize()  # inputs ready: only the plan copy is left in flight
+    side = torch.cuda.Stream(dev)
+    for rep in range(3):
+        p = attn.plan(q_indptr=wl.q_indptr, q_offset=wl.q_offset, kv_len=wl.kv_len,
+                      page_indptr=wl.page_indptr, page_ids=wl.page_ids, num_q_heads=8, num_kv_heads=2,
+                      head_dim=128, num_pool_pages=wl.num_pool_pages, sm_scale=wl.sm_scale,
+                      force_kv_splits=2, device=dev)
+        with torch.cuda.stream(side):
+            out, lse = attn.forward(p, t["q"], t["k_new"], t["v_new"], t["k_cache"], t["v_cache"],
+                                    t["page_ids"], stream=side)
+        side.synchronize()
+        check_full(wl, out, lse)
+
+
 def test_graph_capture_replays(dev):
     """The forward is only kernel launches on the caller's stream, so a HIP
     graph can hold it: every replay (with eager work on the same buffers in
