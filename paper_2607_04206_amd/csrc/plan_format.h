@@ -9,7 +9,7 @@
 namespace sangam {
 
 constexpr uint32_t kPlanMagic = 0x50414753u;  // "SGAP"
-constexpr uint32_t kPlanVersion = 3;
+constexpr uint32_t kPlanVersion = 4;  // 4: prefill_rows may be the wide tile (256)
 
 constexpr int kWaveRows = 32;       // query rows held by one wave (one decode block)
 constexpr int kPrefillQWaves = 4;   // waves of a prefill-shaped work-group

@@ -54,7 +54,7 @@ def test_header_size_matches():
     # plan_format.h static_asserts the same sizes on the C side
     p = plan_of(workloads.tiny_mixed(0))
     h, *_ = parse(p)
-    assert h["magic"] == 0x50414753 and h["version"] == 3
+    assert h["magic"] == 0x50414753 and h["version"] == 4
     assert h["total_bytes"] == p.host.nbytes
     assert HEADER.itemsize == 176 and ITEM.itemsize == 56 and TILE.itemsize == 32
 
