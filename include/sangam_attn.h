@@ -83,7 +83,7 @@ typedef struct sangam_attn_desc {
     int32_t num_cus;         /* compute units to balance over; 0 means 256 */
     const int32_t *q_indptr;    /* [num_items + 1], q_indptr[0] = 0, n_i = q_indptr[i+1]-q_indptr[i] >= 1 */
     const int32_t *q_offset;    /* [num_items] block-offset table o_i >= 0, o_i + n_i <= L_i */
-    const int32_t *kv_len;      /* [num_items] L_i >= 1 */
+    const int32_t *kv_len;      /* [num_items] 1 <= L_i <= 2^30 */
     const int32_t *page_indptr; /* [num_items + 1], page_indptr[i+1]-page_indptr[i] = ceil(L_i/page_size) */
     const int32_t *page_ids;    /* [page_indptr[num_items]], in range, no page twice */
     const int32_t *q_pos;       /* NULL, or [q_indptr[num_items]]: the sequence position of each

@@ -79,6 +79,10 @@ static int64_t min_chunk(int /*qw*/) { return 2048; }
 // the same floor while a decode launch leaves CUs idle (see below)
 static int64_t min_chunk_idle(int qw) { return qw == 1 ? 256 : 512; }
 
+// Longest context an item may have: tile key ranges are int32, and a split's
+// end (its start plus the chunk) must stay representable.
+constexpr int64_t kMaxKvLen = int64_t(1) << 30;
+
 const PlanHeader* check_plan(const void* plan) {
     if (!plan) return nullptr;
     const PlanHeader* h = static_cast<const PlanHeader*>(plan);
@@ -134,8 +138,8 @@ extern "C" sangam_status sangam_attn_plan(const sangam_attn_desc* d, void* plan_
         const int64_t L = d->kv_len[i];
         if (n < 1)
             return fail(SANGAM_ERR_INVALID_ARG, "item " + std::to_string(i) + ": n_i must be >= 1");
-        if (L < 1)
-            return fail(SANGAM_ERR_INVALID_ARG, "item " + std::to_string(i) + ": kv_len must be >= 1");
+        if (L < 1 || L > kMaxKvLen)
+            return fail(SANGAM_ERR_INVALID_ARG, "item " + std::to_string(i) + ": kv_len must be in [1, 2^30]");
         int64_t o = d->q_offset[i];
         if (d->q_pos) {
             const int32_t* pp = d->q_pos + d->q_indptr[i];

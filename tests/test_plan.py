@@ -333,6 +333,15 @@ def test_zero_length_items_rejected():
     _expect("INVALID", **k)
 
 
+def test_context_longer_than_2_30_rejected():
+    """Tile key ranges are int32: a context past 2^30 positions is refused
+    before its page table is read."""
+    k = dict(q_indptr=[0, 32], q_offset=[0], kv_len=[(1 << 30) + 1], page_indptr=[0, 1], page_ids=[0],
+             num_q_heads=1, num_kv_heads=1, head_dim=64, num_pool_pages=4, sm_scale=0.125)
+    _expect("INVALID", **k)
+    assert b"2^30" in lib.sangam_last_error()
+
+
 def test_buffer_too_small_reports_size():
     from paper_2607_04206_amd._lib import SANGAM_OK
     wl = workloads.llada_decode(0)
