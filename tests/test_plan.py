@@ -249,8 +249,38 @@ def test_forced_split_count():
             assert p.workspace_bytes == 0
 
 
-def test_longest_first():
+XCDS = 8
+
+
+def xcd_slots(h, num_cus=256):
+    """Work-group slots per XCD of the prefill-shaped launch."""
+    return max(1, num_cus // XCDS) * (1 if int(h["prefill_rows"]) == 256 else 2)
+
+
+def undo_xcd_order(tiles, C):
+    """The launch order of a long prefill-shaped launch gives XCD x (blocks
+    b = x mod 8) the C consecutive tiles [x C, (x + 1) C) of every chunk of
+    8 C tiles of the longest-first list (a last, partial chunk of M tiles
+    keeps the same layout over M // 8 and its remainder in order). Returns
+    the longest-first list."""
+    out = np.empty_like(tiles)
+    for base in range(0, len(tiles), XCDS * C):
+        M = min(XCDS * C, len(tiles) - base)
+        c = M // XCDS
+        for q in range(M):
+            src = base + XCDS * (q % c) + q // c if q < XCDS * c else base + q
+            out[base + q] = tiles[src]
+    return out
+
+
+def prefill_costs(h, items, pre):
     # cost = keys x waves holding rows (a fused block decode keeps all four busy)
+    waves = int(h["prefill_rows"]) // 32
+    rows = np.minimum(int(h["prefill_rows"]), items["n"][pre["item"]] - pre["row0"])
+    return (pre["kv_end"] - pre["kv_begin"]) * np.where(pre["flags"] & HEADS_ACROSS, waves, (rows + 31) // 32)
+
+
+def test_longest_first():
     for wl in (workloads.dream_mixed(0), workloads.llada_decode(0),
                workloads.make_workload("m", 5, hq=8, hkv=8, d=128, decodes=[(0, 3000), (32, 900)],
                                        prefills=[300, 1000])):
@@ -258,10 +288,49 @@ def test_longest_first():
         h, items, dec, pre, _ = parse(p)
         dc = dec["kv_end"] - dec["kv_begin"]
         assert np.all(np.diff(dc) <= 0)
-        waves = int(h["prefill_rows"]) // 32
-        rows = np.minimum(int(h["prefill_rows"]), items["n"][pre["item"]] - pre["row0"])
-        pc = (pre["kv_end"] - pre["kv_begin"]) * np.where(pre["flags"] & HEADS_ACROSS, waves, (rows + 31) // 32)
-        assert np.all(np.diff(pc) <= 0)
+        assert len(pre) < 8 * XCDS * xcd_slots(h)  # a short launch: plain longest-first order
+        assert np.all(np.diff(prefill_costs(h, items, pre)) <= 0)
+
+
+def test_long_prefill_launch_takes_the_xcd_order():
+    """prefill-heavy (26 rounds of wide tiles): undoing the XCD order gives a
+    longest-first list, and within full chunks an XCD's 32 tiles are row
+    blocks of at most three query heads (19-46 row blocks per head), all but
+    the runs of each head's last, shorter row block, which longest-first
+    order groups across heads."""
+    wl = workloads.prefill_heavy(0)
+    h, items, dec, pre, _ = parse(plan_of(wl))
+    C = xcd_slots(h)
+    assert len(pre) >= 8 * XCDS * C
+    lpt = undo_xcd_order(pre, C)
+    assert np.all(np.diff(prefill_costs(h, items, lpt)) <= 0)
+    assert not np.array_equal(lpt, pre)
+    # the tiles are those of the plain longest-first list, each once
+    key = lambda t: (t["item"], t["q_head0"], t["row0"], t["kv_begin"])
+    assert sorted(map(key, pre)) == sorted(map(key, lpt))
+    runs = local = 0
+    for base in range(0, len(pre) - XCDS * C + 1, XCDS * C):
+        for x in range(XCDS):
+            mine = pre[base + x: base + XCDS * C: XCDS]
+            assert np.array_equal(mine, lpt[base + x * C: base + (x + 1) * C])
+            runs += 1
+            local += len(set(zip(mine["item"], mine["q_head0"]))) <= 3
+    assert local >= 0.95 * runs, (local, runs)
+
+
+@pytest.mark.parametrize("hq,xcd", [(8, False), (16, True)])
+def test_xcd_order_threshold(hq, xcd):
+    """Eight rounds of tiles per slot switch the order: one 2000-row prefill
+    in wide tiles (8 row blocks per head) on 16 CUs (two slots per XCD) gives
+    64 tiles (4 rounds) at 8 heads and 128 (8 rounds) at 16 heads."""
+    wl = workloads.make_workload("xcd", 2, hq=hq, hkv=hq, d=128, decodes=[], prefills=[2000])
+    h, items, dec, pre, _ = parse(plan_of(wl, num_cus=16))
+    assert int(h["prefill_rows"]) == 256 and len(pre) == 8 * hq
+    lpt = undo_xcd_order(pre, xcd_slots(h, 16)) if xcd else pre
+    # longest first, ties in creation order (query head, then row block)
+    cost = prefill_costs(h, items, lpt)
+    assert np.array_equal(np.lexsort((lpt["row0"], lpt["q_head0"], -cost)), np.arange(len(lpt)))
+    assert np.array_equal(lpt, pre) == (not xcd)
 
 
 def test_deterministic_bytes():
