@@ -658,7 +658,7 @@ def bench_workload(args):
         rate = lambda ms: b_d / (ms / 1e3) / 1e9
         measured_peak = ceil["hbm_read_gbs"] if ceil else None
     roof["frac"] = roof["achieved"] / roof["peak"]
-    roof["traffic"] = measured_traffic(wl.name, dom)
+    roof["traffic"] = measured_traffic(args.workload, dom)  # summaries are named by the --workload value
     roof["kernel"] = dom
     roof["kernel_ms"] = dom_ms
     roof["kernel_ms_median"] = float(np.median(dom_all))

@@ -53,3 +53,22 @@ def test_kv_export_oracle_leg():
     r = bench.kv_cpu_baseline(k, v, kv_len, indptr, ids, 2, 64, 5.0)
     assert r["kind"] == "oracle" and r["unit"] == "GB/s" and r["value"] > 0
     assert "90 positions (3 of 3 requests)" in r["sample"]
+
+
+def test_traffic_summaries_are_named_by_workload():
+    """bench.py looks a workload's counter summary up by its --workload name:
+    each profiles/traffic_<name>.json names that workload, which exists."""
+    import glob
+    import json
+    import os
+
+    import workloads
+    files = glob.glob(os.path.join(os.path.dirname(bench.__file__), "profiles", "traffic_*.json"))
+    assert files
+    for f in files:
+        stem = os.path.basename(f)[len("traffic_"):-len(".json")]
+        with open(f) as fh:
+            rec = json.load(fh)
+        assert rec["workload"] == stem and callable(getattr(workloads, stem, None)), f
+        assert rec["kernels"] and all("hbm_bytes_per_launch" in k for k in rec["kernels"].values())
+

@@ -544,7 +544,7 @@ SWEEP_SHAPES = {"llada": (32, 32), "dream": (28, 4)}
 
 def token_cache(seed: int = 0) -> Workload:
     """LLaDA-8B-shaped per-token cached decodes: MHA 32/32, D 128; 32 requests
-    (prompts ~ LN(300, 0.8) in [16, 2048] + 256 response), each recomputing 32
+    (prompts ~ LN(300, 0.8) in [16, 4096] + 256 response), each recomputing 32
     scattered response positions over its whole cached context."""
     return token_cache_decodes(seed, hq=32, hkv=32, d=128, count=32, median=300, sigma=0.8)
 
