@@ -21,7 +21,8 @@
 //                     O^T += V^T P^T directly from the score registers.
 //                     K/V stream global -> LDS with global_load_lds_dwordx4
 //                     into XOR-swizzled tiles (double buffered); V^T operands
-//                     come from ds_read_b64_tr_b16 transposing reads.
+//                     come from ds_read_b64_tr_b16 transposing reads. Output
+//                     rows leave through LDS, whole rows per 16 lanes.
 //   merge_kernel      combines split-context partial (O, LSE) in split order.
 #include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
@@ -649,14 +650,40 @@ __global__ __launch_bounds__(64 * QW * KW, MINB) void attn_tiles_kernel(AttnArgs
     }
 
     // ---- epilogue
+    // Rows written straight to `out` leave through LDS where it holds them:
+    // each lane stages its query's dims in 8-byte pieces, then 16 consecutive
+    // lanes store one whole row in 16-byte pieces (stored directly, one
+    // instruction would leave 16-byte fragments of 32 rows).
+    constexpr int EROW = D * 2 + 16;  // bytes per staged row: 16-byte aligned, shifted by four banks
+    constexpr int EBASE = KW > 1 ? QW * (KW - 1) * MERGE_REGS * 64 * 4 : 0;  // past the merge data
+    constexpr bool ESTAGE = EBASE + QW * QB * 32 * EROW <= 2 * NSTAGE * TILE;
+    const bool split_out = it.num_splits > 1;  // split partials go to the workspace in fp32
+    if constexpr (ESTAGE && KW == 1) {
+        if (!split_out) __syncthreads();  // every wave is past its last stage's reads
+    }
+    uint8_t* ebuf = smem + EBASE + qs * (QB * 32 * EROW);
 #pragma unroll
     for (int qb = 0; qb < QB; ++qb) {
         const int row = row_base + 32 * qb + qn;
         const float l_tot = half_sum(l_run[qb]);
         const float inv = 1.0f / l_tot;
         const float lse_val = m_used[qb] * 0.69314718055994530942f + logf(l_tot);
+        if (ESTAGE && !split_out) {
+#pragma unroll
+            for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+                for (int q4 = 0; q4 < 4; ++q4) {
+                    const int dim = mb * 32 + 8 * q4 + 4 * hh;
+                    const bf16x4 v = {(__bf16)(o[qb][mb][4 * q4] * inv), (__bf16)(o[qb][mb][4 * q4 + 1] * inv),
+                                      (__bf16)(o[qb][mb][4 * q4 + 2] * inv),
+                                      (__bf16)(o[qb][mb][4 * q4 + 3] * inv)};
+                    *(LDS u32x2*)(ebuf + (32 * qb + qn) * EROW + dim * 2) = __builtin_bit_cast(u32x2, v);
+                }
+            if (row < it.n && head_ok && hh == 0 && a.lse) a.lse[(size_t)(it.q_start + row) * a.hq + head] = lse_val;
+            continue;
+        }
         if (row >= it.n || !head_ok) continue;
-        if (it.num_splits > 1) {
+        if (split_out) {
             const size_t prow = (size_t)(t.split * it.n + row) * a.hq + head;
             float* po = a.ws + it.ws_o + prow * D;
 #pragma unroll
@@ -682,6 +709,24 @@ __global__ __launch_bounds__(64 * QW * KW, MINB) void attn_tiles_kernel(AttnArgs
                     *(u32x2*)(op + dim) = __builtin_bit_cast(u32x2, v);
                 }
             if (hh == 0 && a.lse) a.lse[(size_t)(it.q_start + row) * a.hq + head] = lse_val;
+        }
+    }
+    if constexpr (ESTAGE) {
+        if (!split_out && head_ok) {
+            // the wave reads back only rows it staged itself
+            asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+            constexpr int CPR = D / 8;           // 16-byte pieces per row
+            constexpr int NCE = QB * 32 * CPR;   // pieces per wave
+            static_assert(NCE % 64 == 0, "whole rounds of 64 lanes");
+#pragma unroll
+            for (int j = 0; j < NCE / 64; ++j) {
+                const int c = j * 64 + lane;
+                const int r = c / CPR, col = c % CPR;  // staged row r is row row_base + r
+                if (row_base + r < it.n) {
+                    const u32x4 v = *(const LDS u32x4*)(ebuf + r * EROW + col * 16);
+                    *(u32x4*)(a.out + ((size_t)(it.q_start + row_base + r) * a.hq + head) * D + col * 8) = v;
+                }
+            }
         }
     }
 }
