@@ -14,7 +14,7 @@ import workloads
 from tests.test_parity import check_cache, check_full, check_pool_untouched
 from tests.test_plan import parse
 
-N_CASES = 120
+N_CASES = 300
 SHAPES = [(4, 4), (8, 4), (12, 4), (28, 4), (32, 8), (16, 2), (11, 1), (8, 1), (6, 6), (24, 8)]
 
 
