@@ -123,13 +123,29 @@ def test_tiny_mixed(dev, seed):
 
 
 SHAPES = [(4, 4, 64), (8, 2, 64), (18, 2, 64), (28, 4, 128), (32, 32, 128), (8, 4, 128), (11, 1, 128),
-          (24, 8, 128)]
+          (24, 8, 128), (1, 1, 64), (16, 1, 128), (64, 4, 128)]
 
 
 @pytest.mark.parametrize("hq,hkv,d", SHAPES)
 def test_ragged_small(dev, hq, hkv, d):
     wl = workloads.ragged_small(0, hq=hq, hkv=hkv, d=d)
     p, t, out, lse = run(wl, dev)
+    check_full(wl, out, lse)
+    check_cache(wl, t)
+    check_pool_untouched(wl, t)
+
+
+@pytest.mark.parametrize("hq,hkv", [(16, 1), (64, 4)])
+@pytest.mark.parametrize("force", [0, 3])
+def test_large_gqa_group_decode_tiles(dev, hq, hkv, force):
+    """Groups of 16 query heads per KV head in a decode-only batch on 8 CUs
+    (so not the heads-across tiles of a small batch): each group runs as two
+    decode-shaped work-groups of 8 waves, whose outputs take the direct
+    stores (a wave's rows do not fit in LDS beside the stages)."""
+    dec = [(40, 300), (200, 1100), (64, 96), (1000, 9100), (5, 37), (0, 33)]
+    wl = workloads.make_workload("g16", 11, hq=hq, hkv=hkv, d=128, decodes=dec, prefills=[])
+    p, t, out, lse = run(wl, dev, force_splits=force, num_cus=8)
+    assert p.info.num_decode_tiles > 0 and p.info.decode_q_waves == 8 and p.info.num_fused_decode_tiles == 0
     check_full(wl, out, lse)
     check_cache(wl, t)
     check_pool_untouched(wl, t)
